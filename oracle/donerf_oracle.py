@@ -1,0 +1,355 @@
+"""CPU oracle for DONeRF per-ray inference.  TEST INFRASTRUCTURE ONLY.
+
+Only the test suite, the package's smoke check and the benchmark's CPU
+baseline leg may import this module.  The rendering library never calls it.
+The oracle shares no code with the HIP path.
+
+It follows DONeRF (Neff et al., EGSR 2021, arXiv 2103.03231) one step at a time:
+
+  ray through a pixel (Sec. 3, Eq. 1)
+  -> ray unification onto the view-cell sphere (Sec. 4.2, Fig. 8)
+  -> encoded depth-network input, normalised by d_max (Sec. 3, Eq. 2)
+  -> depth-oracle network, 8 linear layers of 256 units (Sec. 4.3, App. D)
+  -> log-discretised depth bins (Sec. 3, Eq. 3; Sec. 4.2) and top-N selection
+  -> samples x = o + t r (Eq. 1) at the selected bin centres
+  -> space warp (Sec. 3, Eq. 4-5) and encoding
+  -> shading network with the encoded direction skipped into its last layer
+     (App. D, Fig. 12)
+  -> alpha compositing with a black background (Sec. 2, Sec. 5.1).
+
+Precision.  Ray geometry (ray, unification, sample placement, warp) runs in
+fp32 with the operation order written below, so that a fp32 implementation
+with the same order reproduces it bit for bit.  Encodings, matrix products
+(fp64 accumulation) and compositing run in fp64.  In ``precision='bf16'`` the
+oracle rounds to bf16 (round-to-nearest-even) exactly where a bf16 network
+does: weights, encoded features and each hidden activation after bias + ReLU.
+Values are first rounded to fp32 and then to bf16.  Logits and head outputs
+stay unrounded.
+
+Readings where the paper is silent are listed in the design document; each
+function names the one it uses.
+
+Every function is pinned by ``tests/test_oracle_pins.py`` against closed
+forms, invariants, the paper's Table 2 and brute force on tiny inputs.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+F32 = np.float32
+HIDDEN = 256
+L_POS = 10
+L_DIR = 4
+
+
+# ---------------------------------------------------------------- rounding
+
+def round_bf16(x) -> np.ndarray:
+    """Round to bf16 (round-to-nearest-even on the fp32 bit pattern), returned
+    as float64 holding the bf16 value.  Values are first rounded to fp32."""
+    f = np.ascontiguousarray(np.asarray(x, dtype=np.float64).astype(F32))
+    u = f.view(np.uint32).astype(np.uint64)
+    lsb = (u >> np.uint64(16)) & np.uint64(1)
+    r = ((u + np.uint64(0x7FFF) + lsb) >> np.uint64(16)) << np.uint64(16)
+    out = (r & np.uint64(0xFFFFFFFF)).astype(np.uint32).view(F32)
+    nan = np.isnan(f)
+    if nan.any():
+        out = np.where(nan, f, out)
+    return out.astype(np.float64)
+
+
+# ---------------------------------------------------------------- depth bins
+
+def log_depth(d, near, far):
+    """Eq. 3: the logarithmic depth map, depth -> network coordinate."""
+    d = np.asarray(d, dtype=np.float64)
+    span = far - near
+    return near + np.log(d - near + 1.0) / np.log(span + 1.0) * span
+
+
+def bin_table(near, far, n_bins):
+    """Depth classes uniform in the log coordinate of Eq. 3 (Sec. 4.2 applies
+    the same transform to the classification steps).
+
+    Boundaries are the inverse of Eq. 3 at B+1 uniform coordinates,
+    b_k = d_min + (D+1)^(k/B) - 1 with b_0 = d_min and b_B = d_max exactly;
+    centres are the inverse at the mid coordinates (k+0.5)/B; widths are
+    b_{k+1} - b_k.  Computed in fp64, returned as fp32.  near/far are taken as
+    fp32 values first (the C ABI stores them as fp32)."""
+    near = float(F32(near))
+    far = float(F32(far))
+    span = far - near
+    k = np.arange(n_bins + 1, dtype=np.float64)
+    b = near + np.power(span + 1.0, k / n_bins) - 1.0
+    b[0] = near
+    b[n_bins] = far
+    kc = np.arange(n_bins, dtype=np.float64) + 0.5
+    c = near + np.power(span + 1.0, kc / n_bins) - 1.0
+    w = b[1:] - b[:-1]
+    return b.astype(F32), c.astype(F32), w.astype(F32)
+
+
+# ---------------------------------------------------------------- geometry (fp32)
+
+def focal_px(W, fov_x_deg):
+    """Pinhole focal length in pixels for a horizontal field of view (fp64,
+    rounded to fp32)."""
+    fov = float(F32(fov_x_deg))
+    return F32((0.5 * W) / math.tan(fov * (math.pi / 180.0) * 0.5))
+
+
+def camera_rays(pose, H, W, fov_x_deg):
+    """Eq. 1's ray o + d r through each pixel centre.  OpenGL camera: the
+    camera looks down its -z axis, +y up, pixel (i, j) with i along the width
+    and j down the image.  Returns o (H*W, 3) and unit r (H*W, 3), fp32,
+    rays in row-major pixel order."""
+    pose = np.asarray(pose, dtype=F32)
+    f = focal_px(W, fov_x_deg)
+    i = np.arange(W, dtype=F32)
+    j = np.arange(H, dtype=F32)
+    u = ((i + F32(0.5)) - F32(0.5 * W)) / f
+    v = -(((j + F32(0.5)) - F32(0.5 * H)) / f)
+    U = np.broadcast_to(u[None, :], (H, W)).reshape(-1)
+    V = np.broadcast_to(v[:, None], (H, W)).reshape(-1)
+    R = pose[:, :3]
+    d = [(R[a, 0] * U + R[a, 1] * V) + R[a, 2] * F32(-1.0) for a in range(3)]
+    n = np.sqrt((d[0] * d[0] + d[1] * d[1]) + d[2] * d[2])
+    r = np.stack([d[0] / n, d[1] / n, d[2] / n], axis=1)
+    o = np.broadcast_to(pose[:, 3], r.shape).astype(F32)
+    return o, r
+
+
+def dot3(a, b):
+    return (a[:, 0] * b[:, 0] + a[:, 1] * b[:, 1]) + a[:, 2] * b[:, 2]
+
+
+def unify(o, r, centre, radius):
+    """Sec. 4.2, Fig. 8: move each ray origin onto the sphere of the given
+    radius around the view-cell centre, along the ray (the forward root of
+    |o + t r - c| = R, clamped at t >= 0; the paper's case of rays looking out
+    of the view cell)."""
+    c = np.asarray(centre, dtype=F32)
+    R = F32(radius)
+    q = o - c
+    b = dot3(r, q)
+    k = dot3(q, q) - R * R
+    disc = np.maximum(b * b - k, F32(0.0))
+    t = np.maximum(-b + np.sqrt(disc), F32(0.0))
+    return o + t[:, None] * r
+
+
+def sample_points(o, r, t):
+    """Eq. 1: x = o + t r for each ray (o, r: (n,3); t: (n, N)) -> (n, N, 3)."""
+    return o[:, None, :] + t[:, :, None] * r[:, None, :]
+
+
+def warp(x, centre, d_max):
+    """Eq. 4-5: p = x - c scaled by W(p) = 1/sqrt(|p| d_max), evaluated as
+    p / sqrt(|p| d_max); the warp of p = 0 is 0."""
+    c = np.asarray(centre, dtype=F32)
+    p = (x - c).astype(F32)
+    n = np.sqrt((p[..., 0] * p[..., 0] + p[..., 1] * p[..., 1]) + p[..., 2] * p[..., 2])
+    s = np.sqrt(n * F32(d_max))
+    with np.errstate(divide="ignore", invalid="ignore"):
+        w = p / s[..., None]
+    return np.where((n == 0)[..., None], F32(0.0), w).astype(F32)
+
+
+# ---------------------------------------------------------------- encoding (fp64)
+
+def encode(v, L):
+    """The paper's encode() (Eq. 2, Eq. 4), read as NeRF's Fourier features
+    with the identity kept: [v, sin(2^0 pi v), cos(2^0 pi v), ...,
+    sin(2^(L-1) pi v), cos(2^(L-1) pi v)], each block over x, y, z.
+    Output 3 + 6L values in fp64."""
+    v = np.asarray(v, dtype=np.float64)
+    out = [v]
+    for k in range(L):
+        a = math.pi * (2.0 ** k) * v
+        out.append(np.sin(a))
+        out.append(np.cos(a))
+    return np.concatenate(out, axis=-1)
+
+
+# ---------------------------------------------------------------- networks
+
+def split_weights(blob, n_bins):
+    """Parse the flat fp32 blob (per layer W[out][in] row-major then b[out];
+    depth network layers 0..7, then shading network layers 0..7) into two
+    lists of (W, b) in fp64.  Shapes follow App. D: 8 layers of 256 units;
+    the depth network maps 90 encoded inputs to n_bins classes; the shading
+    network maps 63 encoded inputs to (r, g, b, sigma) and reads the 27
+    encoded direction values again in its last layer."""
+    dims_in = 3 + 6 * L_POS + 3 + 6 * L_DIR
+    shapes = ([(HIDDEN, dims_in)] + [(HIDDEN, HIDDEN)] * 6 + [(n_bins, HIDDEN)]
+              + [(HIDDEN, 3 + 6 * L_POS)] + [(HIDDEN, HIDDEN)] * 6
+              + [(4, HIDDEN + 3 + 6 * L_DIR)])
+    blob = np.asarray(blob, dtype=F32)
+    layers, off = [], 0
+    for o, i in shapes:
+        W = blob[off:off + o * i].reshape(o, i).astype(np.float64)
+        off += o * i
+        b = blob[off:off + o].astype(np.float64)
+        off += o
+        layers.append((W, b))
+    if off != blob.size:
+        raise ValueError(f"weight blob has {blob.size} values, expected {off}")
+    return layers[:8], layers[8:]
+
+
+def mlp(layers, x, precision="fp64", skip=None):
+    """ReLU MLP: h = ReLU(W_l h + b_l) for every layer but the last, whose
+    output is returned without activation.  ``skip`` (rows x s) is appended to
+    the last layer's input (App. D's single direction skip).  x is (rows, in).
+    In bf16 mode weights, inputs and hidden activations are rounded to bf16;
+    sums accumulate in fp64."""
+    rb = round_bf16 if precision == "bf16" else (lambda a: np.asarray(a, dtype=np.float64))
+    h = rb(x)
+    n = len(layers)
+    for li, (W, b) in enumerate(layers):
+        if li == n - 1 and skip is not None:
+            h = np.concatenate([h, rb(skip)], axis=1)
+        y = h @ rb(W).T + b
+        if li < n - 1:
+            h = rb(np.maximum(y, 0.0))
+        else:
+            h = y
+    return h
+
+
+# ---------------------------------------------------------------- selection
+
+def topn(logits, N):
+    """The N highest-scoring depth classes per ray, ordered by (score desc,
+    index asc), then returned in ascending index order (= depth order).  -0
+    and +0 compare equal; NaN ranks below every number."""
+    logits = np.asarray(logits, dtype=F32)
+    nanmask = np.isnan(logits)
+    key = np.where(nanmask, -np.inf, logits).astype(np.float64)
+    # np.lexsort is stable: among equal scores the lower index stays first.
+    # Primary key: descending score; secondary: NaN after every number.
+    order = np.lexsort((nanmask, -key), axis=-1)
+    return np.sort(order[:, :N], axis=1).astype(np.int32)
+
+
+def softmax_fp32(logits):
+    """Softmax over the classes in fp32: subtract the row maximum, exponentiate,
+    sum in class order, divide.  Strictly monotone, so the top-N of the
+    probabilities is the top-N of the logits."""
+    x = np.asarray(logits, dtype=F32)
+    m = x.max(axis=1, keepdims=True)
+    e = np.exp(x - m).astype(F32)
+    s = np.zeros((x.shape[0], 1), dtype=F32)
+    for k in range(x.shape[1]):
+        s = (s + e[:, k:k + 1]).astype(F32)
+    return (e / s).astype(F32)
+
+
+# ---------------------------------------------------------------- compositing
+
+def composite(raw, t, delta):
+    """NeRF-style accumulation with a black background (Sec. 2, Sec. 5.1).
+
+    raw: (rays, N, 4) network outputs (r, g, b, sigma) in depth order;
+    t, delta: (rays, N) sample depth and the width of its depth class.
+    rgb = sigmoid, sigma = ReLU, tau = sigma * delta, alpha = 1 - exp(-tau),
+    T_0 = 1, T_{i+1} = T_i exp(-tau_i), w_i = T_i alpha_i,
+    C = sum w_i rgb_i, depth = sum w_i t_i.  fp64."""
+    raw = np.asarray(raw, dtype=np.float64)
+    rgb = 1.0 / (1.0 + np.exp(-raw[..., :3]))
+    sigma = np.maximum(raw[..., 3], 0.0)
+    tau = sigma * np.asarray(delta, dtype=np.float64)
+    alpha = -np.expm1(-tau)
+    T = np.ones(raw.shape[0])
+    C = np.zeros((raw.shape[0], 3))
+    D = np.zeros(raw.shape[0])
+    W = np.zeros(raw.shape[:2])
+    for i in range(raw.shape[1]):
+        w = T * alpha[:, i]
+        W[:, i] = w
+        C += w[:, None] * rgb[:, i]
+        D += w * np.asarray(t, dtype=np.float64)[:, i]
+        T = T * np.exp(-tau[:, i])
+    return C, D, W
+
+
+# ---------------------------------------------------------------- full path
+
+def render_rays(d_layers, s_layers, o, r, N, near, far, n_bins, centre, radius,
+                precision="fp64", select="topn", forced_bins=None):
+    """Per-ray inference for rays (o, r) (fp32, (n, 3)).  Returns dict with
+    rgb (n,3), depth (n,), bins (n,N) int32, logits (n,B) fp64 and, for
+    select='topn_softmax', probs (n,B) fp32."""
+    d_max = F32(far)
+    c = np.asarray(centre, dtype=F32)
+    # 1-2: unification and the encoded depth-network input (Eq. 2 / Sec. 4.2).
+    ou = unify(o, r, c, radius)
+    v = ((ou - c) / d_max).astype(F32)
+    enc_r = encode(r, L_DIR)
+    x0 = np.concatenate([encode(v, L_POS), enc_r], axis=1)
+    # 3: depth oracle network -> class scores.
+    logits = mlp(d_layers, x0, precision)
+    out = {"logits": logits}
+    # 4: selection of N classes.
+    lg32 = logits.astype(F32)
+    if select == "topn_softmax":
+        out["probs"] = softmax_fp32(lg32)
+    elif select != "topn":
+        raise ValueError(select)
+    bins = topn(lg32, N) if forced_bins is None else np.asarray(forced_bins, dtype=np.int32)
+    out["bins"] = bins
+    # 5: samples at the selected class centres (Eq. 1, Eq. 3).
+    _, centres, widths = bin_table(near, far, n_bins)
+    t = centres[bins]
+    delta = widths[bins]
+    x = sample_points(o, r, t).astype(F32)
+    # 6: space warp (Eq. 4-5) and encoding.
+    w = warp(x, c, d_max)
+    n = o.shape[0]
+    feats = encode(w.reshape(n * N, 3), L_POS)
+    skip = np.repeat(enc_r, N, axis=0)
+    raw = mlp(s_layers, feats, precision, skip=skip).reshape(n, N, 4)
+    # 7: compositing.
+    C, D, _ = composite(raw, t, delta)
+    out["rgb"] = C
+    out["depth"] = D
+    return out
+
+
+def render(weights, poses, H, W, N, n_bins=128, near=0.1, far=10.0, fov_x_deg=60.0,
+           centre=(0.0, 0.0, 0.0), radius=1.5, precision="fp64", select="topn",
+           forced_bins=None, ray_subset=None, chunk=8192):
+    """Render P poses (P, 3, 4) of H x W rays.  Returns rgb (P*H*W, 3), depth,
+    bins and logits for every ray (or for ``ray_subset``, global ray ids)."""
+    d_layers, s_layers = split_weights(weights, n_bins)
+    poses = np.asarray(poses, dtype=F32).reshape(-1, 3, 4)
+    os_, rs_ = [], []
+    for p in poses:
+        o, r = camera_rays(p, H, W, fov_x_deg)
+        os_.append(o)
+        rs_.append(r)
+    o = np.concatenate(os_)
+    r = np.concatenate(rs_)
+    ids = np.arange(o.shape[0]) if ray_subset is None else np.asarray(ray_subset)
+    fb = None if forced_bins is None else np.asarray(forced_bins)
+    res = {}
+    for s in range(0, len(ids), chunk):
+        sl = ids[s:s + chunk]
+        part = render_rays(d_layers, s_layers, o[sl], r[sl], N, near, far, n_bins,
+                           centre, radius, precision, select,
+                           None if fb is None else fb[s:s + chunk])
+        for k, val in part.items():
+            res.setdefault(k, []).append(val)
+    return {k: np.concatenate(v) for k, v in res.items()}
+
+
+# ---------------------------------------------------------------- analytic cost
+
+def mlp_macs_per_ray(N, n_bins=128, d_in=90, s_in=63, skip=27, width=HIDDEN):
+    """Multiply-adds of both networks for one ray with N samples (App. D's
+    8-layer architecture): depth network once, shading network N times."""
+    d = d_in * width + 6 * width * width + width * n_bins
+    s = s_in * width + 6 * width * width + (width + skip) * 4
+    return d + N * s
