@@ -1,0 +1,159 @@
+"""Benchmark: DONeRF per-ray inference, 400x400 frames, N = 4, bf16 networks.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                    [--cpu-sample RAYS | --no-cpu]
+
+One step renders the workload's 5 seeded poses (5 x 400 x 400 = 800,000 rays)
+with one donerf_render call (one kernel launch) on inputs already resident:
+weights on the device since donerf_create, poses passed by value.  Prints one
+JSON line.  The roofline object is for the fused render kernel; its time is
+measured with HIP events on the stream the kernel runs on.  The CPU baseline
+is the oracle (bf16-rounding mode) timed on a seeded sample of the same rays.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}   # MI355X dense peaks
+HBM_PEAK_GBS = 8000.0
+
+
+def algorithmic_flop_per_ray(N: int, n_bins: int) -> int:
+    """2 x multiply-adds of both networks for one ray (8 layers of 256 units):
+    depth network 90->256, 6 x 256->256, 256->B once; shading network
+    63->256, 6 x 256->256, 283->4 for each of the N samples."""
+    d = 90 * 256 + 6 * 256 * 256 + 256 * n_bins
+    s = 63 * 256 + 6 * 256 * 256 + (256 + 27) * 4
+    return 2 * (d + N * s)
+
+
+def padded_flop_per_ray(N: int, n_bins: int) -> int:
+    """2 x multiply-adds the MFMA tiles execute (K padded to 96 / 64 / 288,
+    shading head padded to 32 rows)."""
+    d = 96 * 256 + 6 * 256 * 256 + 256 * n_bins
+    s = 64 * 256 + 6 * 256 * 256 + 288 * 32
+    return 2 * (d + N * s)
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(wl, weights, poses, n_sample):
+    from threadpoolctl import threadpool_info
+
+    from oracle import donerf_oracle as O
+    rng = np.random.default_rng(1234)
+    total = wl.rays
+    sub = np.sort(rng.choice(total, size=min(n_sample, total), replace=False))
+    log(f"cpu baseline: oracle ({wl.precision}) on {len(sub)} sampled rays")
+    t0 = time.perf_counter()
+    O.render(weights, poses, wl.H, wl.W, wl.N, n_bins=wl.n_bins, fov_x_deg=wl.fov_deg,
+             precision=wl.precision, ray_subset=sub)
+    dt = time.perf_counter() - t0
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {"value": len(sub) / dt / 1e6, "unit": "Mrays/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{len(sub)} rays drawn uniformly (seed 1234) from the {wl.n_poses} x {wl.H} x "
+                      f"{wl.W} workload, {wl.precision}-rounding oracle, {dt:.1f} s; "
+                      f"os.cpu_count()={os.cpu_count()}"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="frame400_n4_bf16")
+    ap.add_argument("--cpu-sample", type=int, default=262144)
+    ap.add_argument("--no-cpu", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only: the rays of a frame are "
+                                   "independent, so several GPUs would each render a share of the "
+                                   "image; only --gpus 1 is measured"}))
+        sys.exit(2)
+
+    import torch
+
+    from paper_2103_03231_amd import binding as b
+    from paper_2103_03231_amd import inputs
+
+    wl = inputs.WORKLOADS[args.workload]
+    weights = inputs.make_weights(wl.n_bins, 0)
+    poses = wl.poses()
+    P = len(poses)
+    prec = b.BF16 if wl.precision == "bf16" else b.FP32
+    sel = b.SELECT_TOPN_SOFTMAX if wl.select == "topn_softmax" else b.SELECT_TOPN
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    r = b.Renderer(b.Config(n_bins=wl.n_bins, n_max=wl.N, precision=prec, fov_x_deg=wl.fov_deg,
+                            select=sel), weights)
+    out = r.alloc(P, wl.H, wl.W, wl.N, depth=wl.want_depth)
+    log(f"workload {wl.name}: {P} x {wl.H} x {wl.W} rays, N={wl.N}, B={wl.n_bins}, {wl.precision}")
+
+    for _ in range(args.warmup):
+        r.render_into(poses, wl.H, wl.W, wl.N, out)
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} steps)")
+
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for e0, e1 in ev:
+        e0.record(stream)
+        r.render_into(poses, wl.H, wl.W, wl.N, out)
+        e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kern_ms = [e0.elapsed_time(e1) for e0, e1 in ev]
+    avg_kern_ms = float(np.mean(kern_ms))
+    log(f"timed {args.steps} steps: wall {wall * 1e3:.2f} ms, kernel avg {avg_kern_ms:.4f} ms")
+
+    rays = wl.rays
+    ms_step = wall * 1e3 / args.steps
+    value = rays / (ms_step * 1e-3) / 1e6
+    flop_launch = algorithmic_flop_per_ray(wl.N, wl.n_bins) * rays
+    achieved = flop_launch / (avg_kern_ms * 1e-3) / 1e12
+    peak = MFMA_PEAK_TFLOPS[wl.precision]
+    paper_mrays = 400 * 400 / 22e-3 / 1e6   # 22 ms per 400x400 frame, N = 4
+    line = {
+        "metric": "Mrays/s + ms/frame at 400x400 N=4 (8x256 MLPs); MFMA util % of peak",
+        "value": round(value, 3),
+        "unit": "Mrays/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "ms_per_frame": round(ms_step / P, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": round(value / paper_mrays, 2) if wl.name == "frame400_n4_bf16" else None,
+        "dtype": wl.precision,
+        "data": "synthetic: seeded cameras on a sphere of radius 1.5 looking at the origin, "
+                "He-uniform random-init weights (SplitMix64 seed 0)",
+        "config": {"workload": wl.name, "poses": P, "H": wl.H, "W": wl.W, "samples_per_ray": wl.N,
+                   "depth_classes": wl.n_bins, "rays_per_step": rays,
+                   "algorithmic_mflop_per_ray": round(algorithmic_flop_per_ray(wl.N, wl.n_bins) / 1e6, 4),
+                   "padded_mflop_per_ray": round(padded_flop_per_ray(wl.N, wl.n_bins) / 1e6, 4)},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(achieved / peak, 4), "traffic": None,
+                     "kernel": "render_kernel<bf16>", "kernel_ms": round(avg_kern_ms, 4)},
+    }
+    if not args.no_cpu:
+        line["cpu_baseline"] = cpu_baseline(wl, weights, poses, args.cpu_sample)
+    r.close()
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

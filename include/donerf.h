@@ -1,0 +1,185 @@
+/*
+ * donerf.h - C ABI of the DONeRF per-ray inference library for MI355X (gfx950).
+ *
+ * The library renders camera images with DONeRF (Neff et al., "DONeRF: Towards
+ * Real-Time Rendering of Compact Neural Radiance Fields using Depth Oracle
+ * Networks", EGSR 2021).  For every pixel ray (Sec. 3, Eq. 1) it
+ *   1. moves the ray origin onto the sphere around the view cell (Sec. 4.2),
+ *   2. evaluates the depth-oracle network once on the encoded unified origin
+ *      and direction, giving one score per logarithmic depth class (Sec. 4.1,
+ *      Eq. 3 discretisation),
+ *   3. keeps the N best-scoring classes and places one sample at the centre
+ *      of each (Eq. 1 with the class centre as depth),
+ *   4. warps each sample towards the view cell (Eq. 4-5) and encodes it,
+ *   5. evaluates the shading network at the N samples, with the encoded ray
+ *      direction fed again into its last layer (App. D), and
+ *   6. alpha-composites the N samples front to back over a black background.
+ * Both networks have 8 linear layers of 256 units with ReLU (App. D).
+ *
+ * Conventions
+ *   - All functions return a donerf_status; 0 is success.
+ *   - Every argument is validated before any HIP call, so invalid arguments
+ *     are reported without touching the GPU.
+ *   - Pointers documented as "host" are read during the call only; pointers
+ *     documented as "device" must be device memory of the current HIP device
+ *     and are accessed asynchronously on the handle's stream.
+ *   - A handle is not reentrant: one render in flight per handle at a time.
+ *   - The message of the most recent failure in the calling thread is kept in
+ *     donerf_last_error().
+ */
+#ifndef DONERF_H
+#define DONERF_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct donerf_handle donerf_t;
+
+typedef enum donerf_status {
+    DONERF_OK = 0,
+    DONERF_E_INVALID_ARG = -1, /* NULL pointer, size or enum out of range    */
+    DONERF_E_SIZE = -2,        /* weight count does not match the config     */
+    DONERF_E_NONFINITE = -3,   /* NaN or Inf in weights, poses or config     */
+    DONERF_E_DEVICE = -4,      /* no HIP device, or the device is not gfx950 */
+    DONERF_E_NOMEM = -5,       /* device or host allocation failed           */
+    DONERF_E_HIP = -6,         /* a HIP call failed; see donerf_last_error() */
+    DONERF_E_UNSUPPORTED = -7  /* valid request this build does not handle   */
+} donerf_status;
+
+typedef enum donerf_precision {
+    DONERF_FP32 = 0, /* fp32 weights, features and activations, fp32 MFMA    */
+    DONERF_BF16 = 1  /* bf16 weights, features and hidden activations (RNE),
+                        fp32 accumulation, fp32 scores, heads, compositing   */
+} donerf_precision;
+
+typedef enum donerf_select {
+    DONERF_SELECT_TOPN = 0,        /* N highest class scores                   */
+    DONERF_SELECT_TOPN_SOFTMAX = 1 /* the same classes, ranked on the softmax of
+                                      the scores (strictly monotone, so the
+                                      selection equals DONERF_SELECT_TOPN)     */
+} donerf_select;
+
+/* Maximum number of samples per ray a handle can be created for. */
+#define DONERF_MAX_SAMPLES 16
+
+typedef struct donerf_cfg {
+    float near_dist;   /* d_min > 0: nearest sample depth along the ray (Eq. 1) */
+    float far_dist;    /* d_max > d_min: farthest depth; also the normalisation
+                          of Eq. 2 and the warp scale of Eq. 5                 */
+    int32_t n_bins;    /* B: number of logarithmic depth classes (Eq. 3);
+                          this build supports 64, 128, 192 and 256            */
+    int32_t n_max;     /* largest N a render may request, 1..16, n_max <= B   */
+    float fov_x_deg;   /* horizontal field of view of the pinhole camera, in
+                          degrees, 0 < fov < 180                               */
+    float centre[3];   /* view-cell centre c (Eq. 2, Eq. 4)                    */
+    float radius;      /* radius > 0 of the unification sphere (Sec. 4.2)      */
+    int32_t precision; /* donerf_precision                                     */
+    int32_t select;    /* donerf_select                                        */
+} donerf_cfg;
+
+/*
+ * Number of fp32 values in the weight blob for B depth classes, or 0 if B is
+ * not positive.
+ *
+ * Blob layout (host, fp32): depth network layers 0..7, then shading network
+ * layers 0..7; each layer is W[out][in] row-major followed by b[out].
+ *   depth  : 90 -> 256, 6 x (256 -> 256), 256 -> B
+ *   shading: 63 -> 256, 6 x (256 -> 256), (256 + 27) -> 4
+ * Depth layer 0 reads the encoding of the unified origin divided by d_max
+ * (63 values) followed by the encoding of the direction (27 values).  The
+ * encoding of v with L frequencies is [v, sin(2^0 pi v), cos(2^0 pi v), ...,
+ * sin(2^(L-1) pi v), cos(2^(L-1) pi v)], each block over x, y, z; L = 10 for
+ * positions, 4 for directions.  Shading layer 0 reads the encoding of the
+ * warped sample (63); shading layer 7 reads the 256 hidden values followed by
+ * the direction encoding (27) and outputs (r, g, b, sigma) before activation.
+ */
+size_t donerf_weight_count(int32_t n_bins);
+
+/*
+ * Create a renderer on the current HIP device.
+ *   cfg       host, read during the call
+ *   weights   host fp32 blob of n_weights values (layout above); the library
+ *             converts and copies it to the device, so the caller may free it
+ *             on return
+ *   out       receives the handle; set to NULL on failure
+ * Errors: E_INVALID_ARG (NULL, cfg ranges), E_UNSUPPORTED (n_bins not in the
+ * supported set), E_SIZE (n_weights != donerf_weight_count(cfg->n_bins)),
+ * E_NONFINITE (NaN/Inf in cfg or weights), E_DEVICE (no device or not
+ * gfx950), E_NOMEM, E_HIP.
+ */
+int donerf_create(const donerf_cfg* cfg, const float* weights, size_t n_weights,
+                  donerf_t** out);
+
+/* Release the handle and its device memory.  NULL is allowed. */
+void donerf_destroy(donerf_t* h);
+
+/*
+ * Bind the HIP stream (a hipStream_t passed as void*) on which the handle's
+ * work is enqueued.  NULL selects the null stream (the default).
+ */
+int donerf_set_stream(donerf_t* h, void* stream);
+
+/*
+ * Render P camera images of H x W pixels with N samples per ray.
+ *   cam_poses  host, P x 12 fp32: camera-to-world 3x4 row-major [R | o] per
+ *              image; the camera looks down its -z axis, +y is up; pixel
+ *              (i, j), i along the width and j downwards, is the ray through
+ *              the pixel centre
+ *   N          samples per ray, 1 <= N <= cfg.n_max (and <= B)
+ *   out_rgb    device, P x H x W x 3 fp32, row-major, caller-owned
+ *   out_depth  device, P x H x W fp32 (sum of sample weight x sample depth),
+ *              or NULL to skip
+ * The work is enqueued on the handle's stream; results are valid once the
+ * stream has been synchronised.  No allocation, no host synchronisation.
+ * Errors: E_INVALID_ARG (NULL handle/poses/out_rgb, P, H, W < 1, N out of
+ * range, P*H*W >= 2^31), E_NONFINITE (pose), E_HIP (launch failed).
+ */
+int donerf_render(donerf_t* h, const float* cam_poses, int32_t P, int32_t H, int32_t W,
+                  int32_t N, float* out_rgb, float* out_depth);
+
+/*
+ * donerf_render with optional per-ray intermediate outputs, for testing.
+ *   out_bins    device, P x H x W x N int32: the selected depth classes in
+ *               ascending order (= sample order), or NULL
+ *   out_scores  device, P x H x W x B fp32: depth-network scores, or NULL;
+ *               with DONERF_SELECT_TOPN_SOFTMAX the softmax probabilities
+ * Same errors as donerf_render.
+ */
+int donerf_render_debug(donerf_t* h, const float* cam_poses, int32_t P, int32_t H,
+                        int32_t W, int32_t N, float* out_rgb, float* out_depth,
+                        int32_t* out_bins, float* out_scores);
+
+/*
+ * Run the device top-N selection on given scores, for testing.
+ *   scores   device, rays x B fp32, finite
+ *   out_idx  device, rays x N int32: the N classes with the highest scores,
+ *            ties broken towards the lower class index, +0 and -0 equal,
+ *            written in ascending class order
+ * Errors: E_INVALID_ARG (NULL, rays < 1, N out of range), E_HIP.
+ */
+int donerf_debug_topn(donerf_t* h, const float* scores, int32_t rays, int32_t N,
+                      int32_t* out_idx);
+
+/*
+ * Copy the handle's depth-class table to host memory: bounds (B + 1 values,
+ * may be NULL), centres (B), widths (B).  Bounds b_k = d_min + (d_max - d_min
+ * + 1)^(k/B) - 1 (the inverse of Eq. 3 on a uniform grid), centres at
+ * (k + 0.5)/B, widths b_{k+1} - b_k; computed in fp64, stored as fp32.
+ */
+int donerf_debug_bins(const donerf_t* h, float* bounds, float* centres, float* widths);
+
+/* Static description of a status code. */
+const char* donerf_status_str(int status);
+
+/* Message of the most recent failure in the calling thread ("" if none). */
+const char* donerf_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DONERF_H */

@@ -325,18 +325,19 @@ def render(weights, poses, H, W, N, n_bins=128, near=0.1, far=10.0, fov_x_deg=60
     bins and logits for every ray (or for ``ray_subset``, global ray ids)."""
     d_layers, s_layers = split_weights(weights, n_bins)
     poses = np.asarray(poses, dtype=F32).reshape(-1, 3, 4)
-    os_, rs_ = [], []
-    for p in poses:
-        o, r = camera_rays(p, H, W, fov_x_deg)
-        os_.append(o)
-        rs_.append(r)
-    o = np.concatenate(os_)
-    r = np.concatenate(rs_)
-    ids = np.arange(o.shape[0]) if ray_subset is None else np.asarray(ray_subset)
+    hw = H * W
+    ids = np.arange(len(poses) * hw) if ray_subset is None else np.asarray(ray_subset, dtype=np.int64)
+    o = np.empty((len(ids), 3), F32)
+    r = np.empty((len(ids), 3), F32)
+    for pi in np.unique(ids // hw):
+        sel = np.nonzero(ids // hw == pi)[0]
+        po, pr = camera_rays(poses[pi], H, W, fov_x_deg)
+        o[sel] = po[ids[sel] - pi * hw]
+        r[sel] = pr[ids[sel] - pi * hw]
     fb = None if forced_bins is None else np.asarray(forced_bins)
     res = {}
     for s in range(0, len(ids), chunk):
-        sl = ids[s:s + chunk]
+        sl = slice(s, s + chunk)
         part = render_rays(d_layers, s_layers, o[sl], r[sl], N, near, far, n_bins,
                            centre, radius, precision, select,
                            None if fb is None else fb[s:s + chunk])

@@ -1,0 +1,370 @@
+// host.cpp - the C ABI of include/donerf.h: validation, depth-class table,
+// weight packing into the kernels' fragment stream, launches.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/donerf.h"
+#include "internal.h"
+#include "layout.h"
+
+using namespace donerf;
+
+struct donerf_handle {
+    donerf_cfg cfg;
+    bool bf16;
+    int device;
+    hipStream_t stream;
+    void* d_frags;       // device: depth stream then shading stream
+    float* bias;         // device
+    float* bins;         // device: centres[B], widths[B]
+    int n_d_chunks, n_s_chunks, bias_len;
+    std::vector<float> h_bounds, h_centres, h_widths;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string& msg) {
+    g_err = msg;
+    return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+    return fail(DONERF_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+bool finite(float x) { return std::isfinite(x); }
+
+const int kKinds[16] = {kDFirst, kHiddenL, kHiddenL, kHiddenL, kHiddenL, kHiddenL, kHiddenL, kDHead,
+                        kSFirst, kHiddenL, kHiddenL, kHiddenL, kHiddenL, kHiddenL, kHiddenL, kSHead};
+
+bool bins_supported(int B) { return B >= 64 && B <= 256 && B % 64 == 0; }
+
+int validate_cfg(const donerf_cfg* c) {
+    if (!c) return fail(DONERF_E_INVALID_ARG, "cfg is NULL");
+    const float fs[] = {c->near_dist, c->far_dist, c->fov_x_deg, c->centre[0], c->centre[1],
+                        c->centre[2], c->radius};
+    for (float f : fs)
+        if (!finite(f)) return fail(DONERF_E_NONFINITE, "cfg holds a NaN or Inf");
+    if (!(c->near_dist > 0.0f)) return fail(DONERF_E_INVALID_ARG, "near_dist must be > 0");
+    if (!(c->far_dist > c->near_dist)) return fail(DONERF_E_INVALID_ARG, "far_dist must exceed near_dist");
+    if (!(c->fov_x_deg > 0.0f && c->fov_x_deg < 180.0f))
+        return fail(DONERF_E_INVALID_ARG, "fov_x_deg must lie in (0, 180)");
+    if (!(c->radius > 0.0f)) return fail(DONERF_E_INVALID_ARG, "radius must be > 0");
+    if (c->n_bins < 1) return fail(DONERF_E_INVALID_ARG, "n_bins must be >= 1");
+    if (c->n_max < 1 || c->n_max > DONERF_MAX_SAMPLES)
+        return fail(DONERF_E_INVALID_ARG, "n_max must lie in [1, 16]");
+    if (c->n_max > c->n_bins) return fail(DONERF_E_INVALID_ARG, "n_max exceeds n_bins");
+    if (c->precision != DONERF_FP32 && c->precision != DONERF_BF16)
+        return fail(DONERF_E_INVALID_ARG, "unknown precision");
+    if (c->select != DONERF_SELECT_TOPN && c->select != DONERF_SELECT_TOPN_SOFTMAX)
+        return fail(DONERF_E_INVALID_ARG, "unknown select mode");
+    if (!bins_supported(c->n_bins))
+        return fail(DONERF_E_UNSUPPORTED, "n_bins must be 64, 128, 192 or 256");
+    return DONERF_OK;
+}
+
+// Inverse of Eq. 3 on the uniform grid of the network coordinate, in fp64.
+void make_bins(const donerf_cfg& c, std::vector<float>& bounds, std::vector<float>& centres,
+               std::vector<float>& widths) {
+    const int B = c.n_bins;
+    const double near = c.near_dist, far = c.far_dist, span = far - near;
+    std::vector<double> b(B + 1);
+    for (int k = 0; k <= B; ++k) b[k] = near + std::pow(span + 1.0, (double)k / B) - 1.0;
+    b[0] = near;
+    b[B] = far;
+    bounds.resize(B + 1);
+    centres.resize(B);
+    widths.resize(B);
+    for (int k = 0; k <= B; ++k) bounds[k] = (float)b[k];
+    for (int k = 0; k < B; ++k) {
+        centres[k] = (float)(near + std::pow(span + 1.0, ((double)k + 0.5) / B) - 1.0);
+        widths[k] = (float)(b[k + 1] - b[k]);
+    }
+}
+
+uint16_t to_bf16(float x) {  // round to nearest even (inputs are finite)
+    uint32_t u;
+    std::memcpy(&u, &x, 4);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+// Logical input column of the blob for K step ks, lane group g, element e.
+int in_col(bool bf16, int kind, int ks, int g, int e) {
+    const int E = elems(bf16);
+    switch (kind) {
+        case kDFirst: return d_feature(g, ks * E + e);
+        case kSFirst: return s_feature(g, ks * E + e);
+        case kHiddenL:
+        case kDHead: return chained_row(bf16, ks, g, e);
+        default: {  // kSHead: chained hidden units, then the direction skip
+            const int ksh = ksteps(bf16, kHidden);
+            if (ks < ksh) return chained_row(bf16, ks, g, e);
+            const int f = skip_feature(g, (ks - ksh) * E + e);
+            return f < 0 ? -1 : kHidden + f;
+        }
+    }
+}
+
+// Append one layer's fragments, in the order the kernel consumes them
+// (pass, K step, row block within the pass), padded to whole chunks.
+void pack_layer(bool bf16, int kind, int n_bins, const float* W, std::vector<uint8_t>& dst) {
+    const LayerGeom lg = layer_geom(kind, n_bins);
+    const int KS = ksteps(bf16, lg.kpad);
+    const int E = elems(bf16);
+    const size_t start = dst.size();
+    dst.resize(start + (size_t)layer_chunks(bf16, kind, n_bins) * kChunkBytes, 0);
+    uint8_t* out = dst.data() + start;
+    size_t f = 0;
+    for (int p = 0; p < lg.rb / lg.rbp; ++p)
+        for (int ks = 0; ks < KS; ++ks)
+            for (int r = 0; r < lg.rbp; ++r, ++f) {
+                const int rb = p * lg.rbp + r;
+                uint8_t* frag = out + f * kFragBytes;
+                for (int lane = 0; lane < 64; ++lane) {
+                    const int row = 32 * rb + lane % 32, g = lane / 32;
+                    for (int e = 0; e < E; ++e) {
+                        const int colx = in_col(bf16, kind, ks, g, e);
+                        const float v = (row < lg.out_rows && colx >= 0) ? W[(size_t)row * lg.in_cols + colx] : 0.0f;
+                        if (bf16) {
+                            const uint16_t h = to_bf16(v);
+                            std::memcpy(frag + lane * 16 + e * 2, &h, 2);
+                        } else {
+                            std::memcpy(frag + lane * 16 + e * 4, &v, 4);
+                        }
+                    }
+                }
+            }
+}
+
+int check_device(int* dev_out) {
+    int n = 0;
+    if (hipGetDeviceCount(&n) != hipSuccess || n < 1) {
+        (void)hipGetLastError();
+        return fail(DONERF_E_DEVICE, "no HIP device");
+    }
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return fail(DONERF_E_DEVICE, "hipGetDevice failed");
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess)
+        return fail(DONERF_E_DEVICE, "hipGetDeviceProperties failed");
+    if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+        return fail(DONERF_E_DEVICE, std::string("device is ") + prop.gcnArchName + ", need gfx950");
+    *dev_out = dev;
+    return DONERF_OK;
+}
+
+int validate_render(const donerf_t* h, const float* poses, int32_t P, int32_t H, int32_t W, int32_t N,
+                    const float* out_rgb) {
+    if (!h) return fail(DONERF_E_INVALID_ARG, "handle is NULL");
+    if (!poses) return fail(DONERF_E_INVALID_ARG, "cam_poses is NULL");
+    if (!out_rgb) return fail(DONERF_E_INVALID_ARG, "out_rgb is NULL");
+    if (P < 1 || H < 1 || W < 1) return fail(DONERF_E_INVALID_ARG, "P, H and W must be >= 1");
+    if (N < 1 || N > h->cfg.n_max || N > h->cfg.n_bins)
+        return fail(DONERF_E_INVALID_ARG, "N must lie in [1, n_max]");
+    if ((int64_t)P * H * W >= ((int64_t)1 << 31)) return fail(DONERF_E_INVALID_ARG, "P*H*W must be < 2^31");
+    if ((int64_t)H * W > (1 << 24)) return fail(DONERF_E_INVALID_ARG, "H*W must be <= 2^24");
+    for (int64_t k = 0; k < (int64_t)P * 12; ++k)
+        if (!finite(poses[k])) return fail(DONERF_E_NONFINITE, "cam_poses holds a NaN or Inf");
+    return DONERF_OK;
+}
+
+int ncap_for(int N) { return N <= 4 ? 4 : N <= 8 ? 8 : 16; }
+
+int render_impl(donerf_t* h, const float* poses, int32_t P, int32_t H, int32_t W, int32_t N, float* out_rgb,
+                float* out_depth, int32_t* out_bins, float* out_scores) {
+    int rc = validate_render(h, poses, P, H, W, N, out_rgb);
+    if (rc) return rc;
+    const donerf_cfg& c = h->cfg;
+    RenderArgs a;
+    std::memset(&a, 0, sizeof a);
+    a.d_frags = static_cast<const uint4*>(h->d_frags);
+    a.s_frags = static_cast<const uint4*>(h->d_frags) + (size_t)h->n_d_chunks * (kChunkBytes / 16);
+    a.bias = h->bias;
+    a.bins = h->bins;
+    a.n_d_chunks = h->n_d_chunks;
+    a.n_s_chunks = h->n_s_chunks;
+    a.bias_len = h->bias_len;
+    a.H = H;
+    a.W = W;
+    a.N = N;
+    a.B = c.n_bins;
+    a.focal = (float)((0.5 * W) / std::tan((double)c.fov_x_deg * (M_PI / 180.0) * 0.5));
+    a.half_w = 0.5f * (float)W;
+    a.half_h = 0.5f * (float)H;
+    a.cx = c.centre[0];
+    a.cy = c.centre[1];
+    a.cz = c.centre[2];
+    a.radius = c.radius;
+    a.dmax = c.far_dist;
+    const size_t hw = (size_t)H * W;
+    for (int32_t p0 = 0; p0 < P; p0 += kMaxPosesPerLaunch) {
+        const int np = P - p0 < kMaxPosesPerLaunch ? P - p0 : kMaxPosesPerLaunch;
+        a.n_poses = np;
+        a.total_rays = (uint32_t)(np * hw);
+        std::memcpy(a.poses, poses + (size_t)p0 * 12, sizeof(float) * 12 * np);
+        a.out_rgb = out_rgb + (size_t)p0 * hw * 3;
+        a.out_depth = out_depth ? out_depth + (size_t)p0 * hw : nullptr;
+        a.out_bins = out_bins ? out_bins + (size_t)p0 * hw * N : nullptr;
+        a.out_scores = out_scores ? out_scores + (size_t)p0 * hw * c.n_bins : nullptr;
+        hipError_t e = launch_render(h->bf16, ncap_for(N), a, h->stream);
+        if (e != hipSuccess) return hip_fail(e, "render launch");
+        if (out_scores && c.select == DONERF_SELECT_TOPN_SOFTMAX) {
+            e = launch_softmax_rows(a.out_scores, a.total_rays, c.n_bins, h->stream);
+            if (e != hipSuccess) return hip_fail(e, "softmax launch");
+        }
+    }
+    return DONERF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t donerf_weight_count(int32_t n_bins) {
+    if (n_bins < 1) return 0;
+    size_t n = 0;
+    for (int l = 0; l < 16; ++l) {
+        const LayerGeom lg = layer_geom(kKinds[l], n_bins);
+        n += (size_t)lg.out_rows * lg.in_cols + lg.out_rows;
+    }
+    return n;
+}
+
+int donerf_create(const donerf_cfg* cfg, const float* weights, size_t n_weights, donerf_t** out) {
+    g_err.clear();
+    if (!out) return fail(DONERF_E_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    int rc = validate_cfg(cfg);
+    if (rc) return rc;
+    if (!weights) return fail(DONERF_E_INVALID_ARG, "weights is NULL");
+    const size_t want = donerf_weight_count(cfg->n_bins);
+    if (n_weights != want)
+        return fail(DONERF_E_SIZE, "weight count " + std::to_string(n_weights) + " != " + std::to_string(want));
+    for (size_t k = 0; k < n_weights; ++k)
+        if (!finite(weights[k])) return fail(DONERF_E_NONFINITE, "weights hold a NaN or Inf");
+    int dev = 0;
+    rc = check_device(&dev);
+    if (rc) return rc;
+
+    const bool bf16 = cfg->precision == DONERF_BF16;
+    const int B = cfg->n_bins;
+    std::vector<uint8_t> frags;
+    std::vector<float> bias;
+    int n_d_chunks = 0, n_s_chunks = 0;
+    size_t off = 0;
+    for (int l = 0; l < 16; ++l) {
+        const int kind = kKinds[l];
+        const LayerGeom lg = layer_geom(kind, B);
+        pack_layer(bf16, kind, B, weights + off, frags);
+        (l < 8 ? n_d_chunks : n_s_chunks) += layer_chunks(bf16, kind, B);
+        off += (size_t)lg.out_rows * lg.in_cols;
+        const size_t b0 = bias.size();
+        bias.resize(b0 + bias_len(kind, B), 0.0f);
+        std::memcpy(bias.data() + b0, weights + off, sizeof(float) * lg.out_rows);
+        off += lg.out_rows;
+    }
+
+    donerf_t* h = new (std::nothrow) donerf_handle();
+    if (!h) return fail(DONERF_E_NOMEM, "host allocation failed");
+    h->cfg = *cfg;
+    h->bf16 = bf16;
+    h->device = dev;
+    h->stream = nullptr;
+    h->n_d_chunks = n_d_chunks;
+    h->n_s_chunks = n_s_chunks;
+    h->bias_len = (int)bias.size();
+    make_bins(*cfg, h->h_bounds, h->h_centres, h->h_widths);
+    std::vector<float> bins(2 * B);
+    std::memcpy(bins.data(), h->h_centres.data(), sizeof(float) * B);
+    std::memcpy(bins.data() + B, h->h_widths.data(), sizeof(float) * B);
+
+    hipError_t e;
+    if ((e = hipMalloc(&h->d_frags, frags.size())) != hipSuccess ||
+        (e = hipMalloc(&h->bias, sizeof(float) * bias.size())) != hipSuccess ||
+        (e = hipMalloc(&h->bins, sizeof(float) * bins.size())) != hipSuccess) {
+        donerf_destroy(h);
+        return fail(DONERF_E_NOMEM, std::string("hipMalloc: ") + hipGetErrorString(e));
+    }
+    if ((e = hipMemcpy(h->d_frags, frags.data(), frags.size(), hipMemcpyHostToDevice)) != hipSuccess ||
+        (e = hipMemcpy(h->bias, bias.data(), sizeof(float) * bias.size(), hipMemcpyHostToDevice)) != hipSuccess ||
+        (e = hipMemcpy(h->bins, bins.data(), sizeof(float) * bins.size(), hipMemcpyHostToDevice)) != hipSuccess) {
+        donerf_destroy(h);
+        return hip_fail(e, "hipMemcpy");
+    }
+    *out = h;
+    return DONERF_OK;
+}
+
+void donerf_destroy(donerf_t* h) {
+    if (!h) return;
+    if (h->d_frags) (void)hipFree(h->d_frags);
+    if (h->bias) (void)hipFree(h->bias);
+    if (h->bins) (void)hipFree(h->bins);
+    delete h;
+}
+
+int donerf_set_stream(donerf_t* h, void* stream) {
+    if (!h) return fail(DONERF_E_INVALID_ARG, "handle is NULL");
+    h->stream = static_cast<hipStream_t>(stream);
+    return DONERF_OK;
+}
+
+int donerf_render(donerf_t* h, const float* cam_poses, int32_t P, int32_t H, int32_t W, int32_t N,
+                  float* out_rgb, float* out_depth) {
+    g_err.clear();
+    return render_impl(h, cam_poses, P, H, W, N, out_rgb, out_depth, nullptr, nullptr);
+}
+
+int donerf_render_debug(donerf_t* h, const float* cam_poses, int32_t P, int32_t H, int32_t W, int32_t N,
+                        float* out_rgb, float* out_depth, int32_t* out_bins, float* out_scores) {
+    g_err.clear();
+    return render_impl(h, cam_poses, P, H, W, N, out_rgb, out_depth, out_bins, out_scores);
+}
+
+int donerf_debug_topn(donerf_t* h, const float* scores, int32_t rays, int32_t N, int32_t* out_idx) {
+    g_err.clear();
+    if (!h) return fail(DONERF_E_INVALID_ARG, "handle is NULL");
+    if (!scores || !out_idx) return fail(DONERF_E_INVALID_ARG, "NULL buffer");
+    if (rays < 1) return fail(DONERF_E_INVALID_ARG, "rays must be >= 1");
+    if (N < 1 || N > h->cfg.n_max || N > h->cfg.n_bins) return fail(DONERF_E_INVALID_ARG, "N out of range");
+    hipError_t e = launch_topn(h->bf16, ncap_for(N), scores, rays, N, h->cfg.n_bins, out_idx, h->stream);
+    if (e != hipSuccess) return hip_fail(e, "topn launch");
+    return DONERF_OK;
+}
+
+int donerf_debug_bins(const donerf_t* h, float* bounds, float* centres, float* widths) {
+    g_err.clear();
+    if (!h) return fail(DONERF_E_INVALID_ARG, "handle is NULL");
+    if (!centres || !widths) return fail(DONERF_E_INVALID_ARG, "NULL buffer");
+    const int B = h->cfg.n_bins;
+    if (bounds) std::memcpy(bounds, h->h_bounds.data(), sizeof(float) * (B + 1));
+    std::memcpy(centres, h->h_centres.data(), sizeof(float) * B);
+    std::memcpy(widths, h->h_widths.data(), sizeof(float) * B);
+    return DONERF_OK;
+}
+
+const char* donerf_status_str(int status) {
+    switch (status) {
+        case DONERF_OK: return "ok";
+        case DONERF_E_INVALID_ARG: return "invalid argument";
+        case DONERF_E_SIZE: return "weight count mismatch";
+        case DONERF_E_NONFINITE: return "non-finite value";
+        case DONERF_E_DEVICE: return "no gfx950 device";
+        case DONERF_E_NOMEM: return "out of memory";
+        case DONERF_E_HIP: return "HIP error";
+        case DONERF_E_UNSUPPORTED: return "unsupported configuration";
+        default: return "unknown status";
+    }
+}
+
+const char* donerf_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,42 @@
+// internal.h - interface between the host planner (host.cpp) and the kernels
+// (kernels.hip).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "layout.h"
+
+namespace donerf {
+
+// Everything one render launch needs, passed by value as the kernel argument.
+struct RenderArgs {
+    const uint4* d_frags;   // depth network fragments, chunk-padded per layer
+    const uint4* s_frags;   // shading network fragments, chunk-padded per layer
+    const float* bias;      // all biases (layout.h bias_len), depth then shading
+    const float* bins;      // centres[B] then widths[B]
+    float* out_rgb;         // rays x 3
+    float* out_depth;       // rays, or null
+    int32_t* out_bins;      // rays x N, or null
+    float* out_scores;      // rays x B, or null
+    int32_t n_d_chunks;
+    int32_t n_s_chunks;
+    int32_t bias_len;       // floats in bias
+    int32_t H, W, n_poses, N, B;
+    uint32_t total_rays;    // n_poses * H * W
+    float focal, half_w, half_h;
+    float cx, cy, cz;
+    float radius;
+    float dmax;
+    float poses[kMaxPosesPerLaunch][12];
+};
+
+// Rays handled by one workgroup.
+inline int rays_per_block(bool bf16) { return kWaves * 32 * (bf16 ? 2 : 1); }
+
+hipError_t launch_render(bool bf16, int ncap, const RenderArgs& a, hipStream_t stream);
+hipError_t launch_softmax_rows(float* scores, uint32_t rows, int B, hipStream_t stream);
+hipError_t launch_topn(bool bf16_layout, int ncap, const float* scores, int32_t rays,
+                       int32_t N, int32_t B, int32_t* out_idx, hipStream_t stream);
+
+}  // namespace donerf

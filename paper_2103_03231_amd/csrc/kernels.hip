@@ -1,0 +1,643 @@
+// kernels.hip - DONeRF per-ray inference for gfx950 (MI355X).
+//
+// One fused kernel renders a tile of rays per workgroup: ray generation and
+// unification (Sec. 4.2), encoding of the depth-network input (Eq. 2), the
+// depth-oracle network (App. D) on MFMA, top-N selection of depth classes in
+// registers, sample placement at the class centres (Eq. 1, Eq. 3), the space
+// warp (Eq. 4-5) and encoding, the shading network on MFMA with the encoded
+// direction skipped into its last layer (App. D), and front-to-back
+// compositing over black.  The only HBM traffic is the streamed weights
+// (L2-resident after first touch) and the output pixels.
+//
+// Work split: 4 waves per workgroup, one wave per SIMD.  Each wave owns
+// 32 * CB rays (the MFMA columns); the workgroup shares one stream of weight
+// fragments through a ring of kRing LDS chunks, so each weight byte read from
+// L2 feeds 4 waves.  Activations never leave the registers: accumulators of
+// layer l become, after bias, ReLU and rounding, the B operand of layer l+1
+// (layout.h explains the K permutation that makes this possible).
+#include <hip/hip_runtime.h>
+
+#include <utility>
+
+#include "internal.h"
+
+namespace donerf {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// ------------------------------------------------------------------ compile-time loops
+
+template <class F, int... I>
+__device__ __forceinline__ void sfor_impl(F& f, std::integer_sequence<int, I...>) {
+    (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void sfor(F&& f) {
+    sfor_impl(f, std::make_integer_sequence<int, N>{});
+}
+#define CV(x) decltype(x)::value
+
+// ------------------------------------------------------------------ precision traits
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    f32x2 v = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
+
+template <bool BF16>
+struct Prec;
+
+template <>
+struct Prec<true> {
+    static constexpr int E = 8;      // K elements per lane per fragment
+    static constexpr int CB = 2;     // 32-column blocks per wave
+    static constexpr int KSPB = 2;   // K steps produced per 32-row block
+    __device__ static __forceinline__ f32x16 mma(u32x4 a, u32x4 b, f32x16 c) {
+        return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                       __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+    }
+    __device__ static __forceinline__ u32x4 pack(const float* f) {
+        return u32x4{pack_bf16x2(f[0], f[1]), pack_bf16x2(f[2], f[3]),
+                     pack_bf16x2(f[4], f[5]), pack_bf16x2(f[6], f[7])};
+    }
+};
+
+template <>
+struct Prec<false> {
+    static constexpr int E = 4;
+    static constexpr int CB = 1;
+    static constexpr int KSPB = 4;
+    __device__ static __forceinline__ f32x16 mma(u32x4 a, u32x4 b, f32x16 c) {
+        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
+        return c;
+    }
+    __device__ static __forceinline__ u32x4 pack(const float* f) {
+        return u32x4{__float_as_uint(f[0]), __float_as_uint(f[1]), __float_as_uint(f[2]),
+                     __float_as_uint(f[3])};
+    }
+};
+
+// ------------------------------------------------------------------ LDS weight stream
+
+__device__ __forceinline__ void lds_barrier() {
+    // Orders LDS traffic only; outstanding global prefetches stay in flight.
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+constexpr int kChunkVec = kChunkBytes / 16;           // u32x4 per chunk
+constexpr int kStagePerThread = kChunkVec / kThreads;  // u32x4 each thread moves per chunk
+
+// The workgroup consumes one logical sequence of chunks: every depth-network
+// chunk, then the shading-network chunks once per sample.  Chunk c+1 is
+// copied into LDS while chunk c is consumed and chunk c+2 is in flight from
+// L2 in registers; one barrier per chunk.
+struct WeightStream {
+    const u32x4* dsrc;
+    const u32x4* ssrc;
+    u32x4* ring;
+    int nd, ns, total;
+    int c;      // chunk being consumed
+    int slot;   // its LDS slot
+    int tid;
+    u32x4 stage[kStagePerThread];
+
+    __device__ __forceinline__ const u32x4* src(int k) const {
+        return k < nd ? dsrc + (size_t)k * kChunkVec : ssrc + (size_t)((k - nd) % ns) * kChunkVec;
+    }
+    __device__ __forceinline__ void load(int k) {
+        if (k < total) {
+            const u32x4* p = src(k) + tid;
+#pragma unroll
+            for (int i = 0; i < kStagePerThread; ++i) stage[i] = p[i * kThreads];
+        }
+    }
+    __device__ __forceinline__ void store(int k) {
+        if (k < total) {
+            u32x4* q = ring + (k % kRing) * kChunkVec + tid;
+#pragma unroll
+            for (int i = 0; i < kStagePerThread; ++i) q[i * kThreads] = stage[i];
+        }
+    }
+    __device__ __forceinline__ void start() {
+        c = -1;
+        slot = kRing - 1;
+        load(0);
+        store(0);
+        load(1);
+    }
+    // Advance to the next chunk: publish chunk c+1, barrier, prefetch c+2.
+    __device__ __forceinline__ void next() {
+        ++c;
+        slot = slot == kRing - 1 ? 0 : slot + 1;
+        store(c + 1);
+        lds_barrier();
+        load(c + 2);
+    }
+    __device__ __forceinline__ u32x4 frag(int i, int lane) const {
+        return ring[slot * kChunkVec + i * 64 + lane];
+    }
+};
+
+// ------------------------------------------------------------------ MFMA layers
+
+// Accumulator initialised with the bias of 32-row block r: lane group g holds
+// rows 8q + 4g + j (q, j = 0..3) in register 4q + j.
+__device__ __forceinline__ f32x16 bias_frag(const float* bias, int g) {
+    f32x16 b;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(bias + 8 * q + 4 * g);
+        b[4 * q + 0] = v[0];
+        b[4 * q + 1] = v[1];
+        b[4 * q + 2] = v[2];
+        b[4 * q + 3] = v[3];
+    }
+    return b;
+}
+
+// One accumulator pass: RBP output row blocks x CB column blocks over KS K
+// steps.  BASE is the index of the pass's first fragment within its layer;
+// layers start on chunk boundaries, so chunk changes are known statically.
+template <bool BF16, int KS, int RBP, int BASE, class GetB, class Epi>
+__device__ __forceinline__ void run_pass(WeightStream& st, int lane, int g, const float* bias,
+                                         GetB& getB, Epi&& epi) {
+    using P = Prec<BF16>;
+    f32x16 acc[RBP][P::CB];
+    sfor<RBP>([&](auto R) {
+        const f32x16 b = bias_frag(bias + 32 * CV(R), g);
+        sfor<P::CB>([&](auto C) { acc[CV(R)][CV(C)] = b; });
+    });
+    sfor<KS>([&](auto K) {
+        sfor<RBP>([&](auto R) {
+            constexpr int idx = BASE + CV(K) * RBP + CV(R);
+            if constexpr (idx % kChunkFrags == 0) st.next();
+            const u32x4 a = st.frag(idx % kChunkFrags, lane);
+            sfor<P::CB>([&](auto C) {
+                acc[CV(R)][CV(C)] = P::mma(a, getB(K, C), acc[CV(R)][CV(C)]);
+            });
+        });
+    });
+    sfor<RBP>([&](auto R) { sfor<P::CB>([&](auto C) { epi(R, C, acc[CV(R)][CV(C)]); }); });
+}
+
+// ReLU, round, and place a 32-row accumulator block as K steps
+// [ks0, ks0 + KSPB) of the next layer's B operand.
+template <bool BF16, int NK, int CB>
+__device__ __forceinline__ void emit_relu(const f32x16& acc, u32x4 (&out)[NK][CB], int ks0, int cb) {
+    using P = Prec<BF16>;
+    float v[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) v[i] = fmaxf(acc[i], 0.0f);
+#pragma unroll
+    for (int h = 0; h < P::KSPB; ++h) out[ks0 + h][cb] = P::pack(v + h * P::E);
+}
+
+// Fully connected ReLU layer with 256 outputs (8 row blocks).
+template <bool BF16, int KS, class GetB>
+__device__ __forceinline__ void hidden_layer(WeightStream& st, int lane, int g, const float* bias,
+                                             GetB&& getB,
+                                             u32x4 (&out)[8 * Prec<BF16>::KSPB][Prec<BF16>::CB]) {
+    using P = Prec<BF16>;
+    sfor<8 / kRbPerPass>([&](auto PI) {
+        constexpr int p = CV(PI);
+        run_pass<BF16, KS, kRbPerPass, p * KS * kRbPerPass>(
+            st, lane, g, bias + 32 * kRbPerPass * p, getB, [&](auto R, auto C, const f32x16& acc) {
+                emit_relu<BF16>(acc, out, (p * kRbPerPass + CV(R)) * P::KSPB, CV(C));
+            });
+    });
+}
+
+// ------------------------------------------------------------------ selection
+
+// Best-first list of (score, class) under the order: higher score first,
+// lower class index first among equal scores.
+template <int NCAP>
+struct TopList {
+    float v[NCAP];
+    int i[NCAP];
+    __device__ __forceinline__ void init() {
+#pragma unroll
+        for (int k = 0; k < NCAP; ++k) {
+            v[k] = -INFINITY;
+            i[k] = 0x7fff;
+        }
+    }
+    __device__ __forceinline__ void place(const bool (&c)[NCAP], float x, int ix) {
+        // c is monotone (c[k] implies c[k+1]); shift the tail down by one.
+#pragma unroll
+        for (int k = NCAP - 1; k > 0; --k) {
+            v[k] = c[k - 1] ? v[k - 1] : (c[k] ? x : v[k]);
+            i[k] = c[k - 1] ? i[k - 1] : (c[k] ? ix : i[k]);
+        }
+        v[0] = c[0] ? x : v[0];
+        i[0] = c[0] ? ix : i[0];
+    }
+    // Insert a class whose index exceeds every index already held.
+    __device__ __forceinline__ void push_ascending(float x, int ix) {
+        bool c[NCAP];
+#pragma unroll
+        for (int k = 0; k < NCAP; ++k) c[k] = x > v[k];
+        place(c, x, ix);
+    }
+    // Insert any class.
+    __device__ __forceinline__ void push(float x, int ix) {
+        bool c[NCAP];
+#pragma unroll
+        for (int k = 0; k < NCAP; ++k) c[k] = x > v[k] || (x == v[k] && ix < i[k]);
+        place(c, x, ix);
+    }
+    // Merge with the list of lane l ^ 32 (the other half of the same ray's
+    // classes); both lanes end with the same list.
+    __device__ __forceinline__ void merge_partner() {
+        float pv[NCAP];
+        int pi[NCAP];
+#pragma unroll
+        for (int k = 0; k < NCAP; ++k) {
+            pv[k] = __shfl_xor(v[k], 32);
+            pi[k] = __shfl_xor(i[k], 32);
+        }
+#pragma unroll
+        for (int k = 0; k < NCAP; ++k) push(pv[k], pi[k]);
+    }
+    // The first N classes in ascending index order in s[0..N), padding after.
+    __device__ __forceinline__ void ascending(int N, int (&s)[NCAP]) const {
+#pragma unroll
+        for (int k = 0; k < NCAP; ++k) s[k] = k < N ? i[k] : 0x7fff;
+#pragma unroll
+        for (int round = 0; round < NCAP; ++round) {
+#pragma unroll
+            for (int k = round & 1; k + 1 < NCAP; k += 2) {
+                const int a = s[k], b = s[k + 1];
+                s[k] = min(a, b);
+                s[k + 1] = max(a, b);
+            }
+        }
+    }
+};
+
+template <int NCAP>
+__device__ __forceinline__ int pick(const int (&s)[NCAP], int k) {
+    int r = s[0];
+#pragma unroll
+    for (int q = 1; q < NCAP; ++q) r = k == q ? s[q] : r;
+    return r;
+}
+
+// ------------------------------------------------------------------ geometry (fp32, fixed order)
+// Built with -ffp-contract=off: every operation below rounds to fp32 in the
+// written order.
+
+struct Ray {
+    float o[3], r[3];
+};
+
+__device__ __forceinline__ Ray camera_ray(const RenderArgs& a, uint32_t ray) {
+    const uint32_t hw = (uint32_t)a.H * (uint32_t)a.W;
+    const uint32_t p = ray / hw;
+    const uint32_t pix = ray - p * hw;
+    const uint32_t j = pix / (uint32_t)a.W;
+    const uint32_t i = pix - j * (uint32_t)a.W;
+    const float u = (((float)i + 0.5f) - a.half_w) / a.focal;
+    const float v = -((((float)j + 0.5f) - a.half_h) / a.focal);
+    const float* M = a.poses[p];
+    float d[3];
+#pragma unroll
+    for (int k = 0; k < 3; ++k) d[k] = (M[4 * k + 0] * u + M[4 * k + 1] * v) + M[4 * k + 2] * -1.0f;
+    const float n = __fsqrt_rn((d[0] * d[0] + d[1] * d[1]) + d[2] * d[2]);
+    Ray out;
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+        out.r[k] = d[k] / n;
+        out.o[k] = M[4 * k + 3];
+    }
+    return out;
+}
+
+// Sec. 4.2: the forward intersection with the sphere |x - c| = R, t >= 0.
+__device__ __forceinline__ void unify(const RenderArgs& a, const Ray& ray, float (&ou)[3]) {
+    const float q0 = ray.o[0] - a.cx, q1 = ray.o[1] - a.cy, q2 = ray.o[2] - a.cz;
+    const float b = (ray.r[0] * q0 + ray.r[1] * q1) + ray.r[2] * q2;
+    const float k = ((q0 * q0 + q1 * q1) + q2 * q2) - a.radius * a.radius;
+    const float disc = fmaxf(b * b - k, 0.0f);
+    const float t = fmaxf(-b + __fsqrt_rn(disc), 0.0f);
+#pragma unroll
+    for (int c = 0; c < 3; ++c) ou[c] = ray.o[c] + t * ray.r[c];
+}
+
+// Eq. 4-5: w = p / sqrt(|p| d_max), p = x - c, w = 0 at p = 0.
+__device__ __forceinline__ void warp(const RenderArgs& a, const float (&x)[3], float (&w)[3]) {
+    const float p0 = x[0] - a.cx, p1 = x[1] - a.cy, p2 = x[2] - a.cz;
+    const float n = __fsqrt_rn((p0 * p0 + p1 * p1) + p2 * p2);
+    const float s = __fsqrt_rn(n * a.dmax);
+    const bool z = n == 0.0f;
+    w[0] = z ? 0.0f : p0 / s;
+    w[1] = z ? 0.0f : p1 / s;
+    w[2] = z ? 0.0f : p2 / s;
+}
+
+// Encoding slots: T frequency pairs 2t + g (t < T) of v, written as
+// [sin x, sin y, sin z, cos x, cos y, cos z] per frequency.  The scale 2^k is
+// exact in fp32 and sincospi avoids multiplying by a rounded pi.
+template <int T>
+__device__ __forceinline__ void fourier(const float (&v)[3], int g, float* f) {
+    const float gs = g ? 2.0f : 1.0f;
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+        const float sc = (float)(1u << (2 * t)) * gs;
+#pragma unroll
+        for (int c = 0; c < 3; ++c) {
+            float s, co;
+            sincospif(v[c] * sc, &s, &co);
+            f[6 * t + c] = s;
+            f[6 * t + 3 + c] = co;
+        }
+    }
+}
+
+// ------------------------------------------------------------------ fused kernel
+
+constexpr int kBiasMax = 7 * 256 + 256 + 7 * 256 + 32;
+
+template <bool BF16, int NCAP>
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+render_kernel(const RenderArgs a) {
+    using P = Prec<BF16>;
+    constexpr int CB = P::CB;
+    constexpr int E = P::E;
+    constexpr int KS_D0 = kDKPad / (2 * E);   // 6 | 12
+    constexpr int KS_H = kHidden / (2 * E);   // 16 | 32
+    constexpr int KS_S0 = kSKPad / (2 * E);   // 4 | 8
+    constexpr int KS_SK = kSkipKPad / (2 * E);// 2 | 4
+
+    __shared__ u32x4 ring[kRing * kChunkVec];
+    __shared__ float bias_s[kBiasMax];
+    __shared__ float bins_s[2 * 256];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int g = lane >> 5;
+    const int col = lane & 31;
+
+    for (int k = tid; k < a.bias_len; k += kThreads) bias_s[k] = a.bias[k];
+    for (int k = tid; k < 2 * a.B; k += kThreads) bins_s[k] = a.bins[k];
+
+    WeightStream st;
+    st.dsrc = reinterpret_cast<const u32x4*>(a.d_frags);
+    st.ssrc = reinterpret_cast<const u32x4*>(a.s_frags);
+    st.ring = ring;
+    st.nd = a.n_d_chunks;
+    st.ns = a.n_s_chunks;
+    st.total = a.n_d_chunks + a.N * a.n_s_chunks;
+    st.tid = tid;
+    st.start();
+
+    // ---- rays of this wave: column col of block cb
+    const uint32_t ray0 = ((uint32_t)blockIdx.x * kWaves + wave) * (32 * CB);
+    uint32_t rid[CB];
+    bool valid[CB];
+    Ray ray[CB];
+    u32x4 din[KS_D0][CB];
+    u32x4 skip[KS_SK][CB];
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) {
+        const uint32_t r = ray0 + 32 * cb + col;
+        valid[cb] = r < a.total_rays;
+        rid[cb] = valid[cb] ? r : a.total_rays - 1;
+        ray[cb] = camera_ray(a, rid[cb]);
+        float ou[3], v[3];
+        unify(a, ray[cb], ou);
+        v[0] = (ou[0] - a.cx) / a.dmax;
+        v[1] = (ou[1] - a.cy) / a.dmax;
+        v[2] = (ou[2] - a.cz) / a.dmax;
+        float f[kDSlots];
+        fourier<5>(v, g, f);
+        fourier<2>(ray[cb].r, g, f + 30);
+        f[42] = g ? ray[cb].r[0] : v[0];
+        f[43] = g ? ray[cb].r[1] : v[1];
+        f[44] = g ? ray[cb].r[2] : v[2];
+        f[45] = f[46] = f[47] = 0.0f;
+#pragma unroll
+        for (int ks = 0; ks < KS_D0; ++ks) din[ks][cb] = P::pack(f + E * ks);
+        float fs[kSkipSlots];
+#pragma unroll
+        for (int k = 0; k < 12; ++k) fs[k] = f[30 + k];
+        fs[12] = g ? 0.0f : ray[cb].r[0];
+        fs[13] = g ? 0.0f : ray[cb].r[1];
+        fs[14] = g ? 0.0f : ray[cb].r[2];
+        fs[15] = 0.0f;
+#pragma unroll
+        for (int ks = 0; ks < KS_SK; ++ks) skip[ks][cb] = P::pack(fs + E * ks);
+    }
+    lds_barrier();  // bias_s / bins_s visible (the stream also barriers)
+
+    // ---- depth-oracle network
+    u32x4 h0[KS_H][CB], h1[KS_H][CB];
+    {
+        auto gin = [&](auto K, auto C) { return din[CV(K)][CV(C)]; };
+        hidden_layer<BF16, KS_D0>(st, lane, g, bias_s, gin, h0);
+    }
+    auto g0 = [&](auto K, auto C) { return h0[CV(K)][CV(C)]; };
+    auto g1 = [&](auto K, auto C) { return h1[CV(K)][CV(C)]; };
+    for (int l = 0; l < 3; ++l) {
+        hidden_layer<BF16, KS_H>(st, lane, g, bias_s + 256 * (1 + 2 * l), g0, h1);
+        hidden_layer<BF16, KS_H>(st, lane, g, bias_s + 256 * (2 + 2 * l), g1, h0);
+    }
+    TopList<NCAP> top[CB];
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) top[cb].init();
+    const int npass = a.B / (32 * kRbPerPass);
+    for (int p = 0; p < npass; ++p) {
+        run_pass<BF16, KS_H, kRbPerPass, 0>(
+            st, lane, g, bias_s + 7 * 256 + 64 * p, g0, [&](auto R, auto C, const f32x16& acc) {
+                const int rowb = 64 * p + 32 * CV(R) + 4 * g;
+#pragma unroll
+                for (int i = 0; i < 16; ++i) top[CV(C)].push_ascending(acc[i], rowb + 8 * (i / 4) + (i % 4));
+                if (a.out_scores) {
+                    float* dst = a.out_scores + (size_t)rid[CV(C)] * a.B;
+#pragma unroll
+                    for (int i = 0; i < 16; ++i)
+                        if (valid[CV(C)]) dst[rowb + 8 * (i / 4) + (i % 4)] = acc[i];
+                }
+            });
+    }
+    int sel[CB][NCAP];
+    sfor<CB>([&](auto C) {
+        top[CV(C)].merge_partner();
+        top[CV(C)].ascending(a.N, sel[CV(C)]);
+    });
+
+    // ---- shading network per sample, composited front to back
+    const int s_bias = 7 * 256 + a.B;
+    float T[CB], Cr[CB], Cg[CB], Cb[CB], Dp[CB];
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) T[cb] = 1.0f, Cr[cb] = Cg[cb] = Cb[cb] = Dp[cb] = 0.0f;
+
+    for (int k = 0; k < a.N; ++k) {
+        u32x4 sin_[KS_S0][CB];
+        float tk[CB], dk[CB];
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb) {
+            // Always a class index for finite scores; clamped so that no
+            // sentinel can address outside the class table.
+            const int bin = min(pick(sel[cb], k), a.B - 1);
+            tk[cb] = bins_s[bin];
+            dk[cb] = bins_s[a.B + bin];
+            float x[3], w[3];
+#pragma unroll
+            for (int c = 0; c < 3; ++c) x[c] = ray[cb].o[c] + tk[cb] * ray[cb].r[c];
+            warp(a, x, w);
+            float f[kSSlots];
+            fourier<5>(w, g, f);
+            f[30] = g ? w[2] : w[0];
+            f[31] = g ? 0.0f : w[1];
+#pragma unroll
+            for (int ks = 0; ks < KS_S0; ++ks) sin_[ks][cb] = P::pack(f + E * ks);
+        }
+        {
+            auto gs = [&](auto K, auto C) { return sin_[CV(K)][CV(C)]; };
+            hidden_layer<BF16, KS_S0>(st, lane, g, bias_s + s_bias, gs, h0);
+        }
+        for (int l = 0; l < 3; ++l) {
+            hidden_layer<BF16, KS_H>(st, lane, g, bias_s + s_bias + 256 * (1 + 2 * l), g0, h1);
+            hidden_layer<BF16, KS_H>(st, lane, g, bias_s + s_bias + 256 * (2 + 2 * l), g1, h0);
+        }
+        auto gh = [&](auto K, auto C) {
+            if constexpr (CV(K) < KS_H) return h0[CV(K)][CV(C)];
+            else return skip[CV(K) - KS_H][CV(C)];
+        };
+        run_pass<BF16, KS_H + KS_SK, 1, 0>(
+            st, lane, g, bias_s + s_bias + 7 * 256, gh, [&](auto R, auto C, const f32x16& acc) {
+                constexpr int cb = CV(C);
+                // lanes of group 0 hold rows 0..3 = (r, g, b, sigma) in registers 0..3
+                const float cr = 1.0f / (1.0f + __expf(-acc[0]));
+                const float cg = 1.0f / (1.0f + __expf(-acc[1]));
+                const float cbl = 1.0f / (1.0f + __expf(-acc[2]));
+                const float sigma = fmaxf(acc[3], 0.0f);
+                const float tau = sigma * dk[cb];
+                const float alpha = -expm1f(-tau);
+                const float wgt = T[cb] * alpha;
+                Cr[cb] += wgt * cr;
+                Cg[cb] += wgt * cg;
+                Cb[cb] += wgt * cbl;
+                Dp[cb] += wgt * tk[cb];
+                T[cb] *= expf(-tau);
+            });
+    }
+
+    // ---- outputs (lane group 0 holds the composited values)
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) {
+        if (g == 0 && valid[cb]) {
+            float* o = a.out_rgb + (size_t)rid[cb] * 3;
+            o[0] = Cr[cb];
+            o[1] = Cg[cb];
+            o[2] = Cb[cb];
+            if (a.out_depth) a.out_depth[rid[cb]] = Dp[cb];
+            if (a.out_bins) {
+                for (int k = 0; k < a.N; ++k) a.out_bins[(size_t)rid[cb] * a.N + k] = pick(sel[cb], k);
+            }
+        }
+    }
+}
+
+// Softmax of each score row in place (fp32: subtract the row maximum,
+// exponentiate, sum in class order, divide).  Used for score dumps only: the
+// softmax is strictly monotone, so it never changes the selection.
+__global__ void softmax_rows_kernel(float* s, uint32_t rows, int B) {
+    const uint32_t r = blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= rows) return;
+    float* x = s + (size_t)r * B;
+    float m = x[0];
+    for (int k = 1; k < B; ++k) m = fmaxf(m, x[k]);
+    float sum = 0.0f;
+    for (int k = 0; k < B; ++k) sum += expf(x[k] - m);
+    for (int k = 0; k < B; ++k) x[k] = expf(x[k] - m) / sum;
+}
+
+// The render kernel's selection on given scores: each lane pushes its classes
+// in the render kernel's register order, then merges with its partner lane.
+template <int CB, int NCAP>
+__global__ void __launch_bounds__(256) topn_kernel(const float* scores, int32_t rays, int32_t N, int32_t B,
+                                                   int32_t* out) {
+    const int lane = threadIdx.x & 63;
+    const int g = lane >> 5;
+    const int col = lane & 31;
+    const int wave = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+    sfor<CB>([&](auto C) {
+        const int32_t r = wave * 32 * CB + 32 * CV(C) + col;
+        const bool valid = r < rays;
+        const float* row = scores + (size_t)(valid ? r : rays - 1) * B;
+        TopList<NCAP> t;
+        t.init();
+        for (int p = 0; p < B / 64; ++p)
+            for (int R = 0; R < 2; ++R)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const int c = 64 * p + 32 * R + 8 * (i / 4) + 4 * g + (i % 4);
+                    t.push_ascending(row[c], c);
+                }
+        t.merge_partner();
+        int s[NCAP];
+        t.ascending(N, s);
+        if (g == 0 && valid)
+            for (int k = 0; k < N; ++k) out[(size_t)r * N + k] = pick(s, k);
+    });
+}
+
+}  // namespace
+
+hipError_t launch_render(bool bf16, int ncap, const RenderArgs& a, hipStream_t stream) {
+    const uint32_t rpb = (uint32_t)rays_per_block(bf16);
+    const dim3 grid((a.total_rays + rpb - 1) / rpb);
+    const dim3 block(kThreads);
+#define DN_LAUNCH(B16, NC) hipLaunchKernelGGL((render_kernel<B16, NC>), grid, block, 0, stream, a)
+    if (bf16) {
+        if (ncap == 4) DN_LAUNCH(true, 4);
+        else if (ncap == 8) DN_LAUNCH(true, 8);
+        else DN_LAUNCH(true, 16);
+    } else {
+        if (ncap == 4) DN_LAUNCH(false, 4);
+        else if (ncap == 8) DN_LAUNCH(false, 8);
+        else DN_LAUNCH(false, 16);
+    }
+#undef DN_LAUNCH
+    return hipGetLastError();
+}
+
+hipError_t launch_softmax_rows(float* scores, uint32_t rows, int B, hipStream_t stream) {
+    hipLaunchKernelGGL(softmax_rows_kernel, dim3((rows + 255) / 256), dim3(256), 0, stream, scores, rows, B);
+    return hipGetLastError();
+}
+
+hipError_t launch_topn(bool bf16_layout, int ncap, const float* scores, int32_t rays, int32_t N,
+                       int32_t B, int32_t* out_idx, hipStream_t stream) {
+    const int cb = bf16_layout ? 2 : 1;
+    const int rays_per_block = 4 * 32 * cb;
+    const dim3 grid((rays + rays_per_block - 1) / rays_per_block);
+#define DN_TOPN(CB, NC) hipLaunchKernelGGL((topn_kernel<CB, NC>), grid, dim3(256), 0, stream, scores, rays, N, B, out_idx)
+    if (cb == 2) {
+        if (ncap == 4) DN_TOPN(2, 4);
+        else if (ncap == 8) DN_TOPN(2, 8);
+        else DN_TOPN(2, 16);
+    } else {
+        if (ncap == 4) DN_TOPN(1, 4);
+        else if (ncap == 8) DN_TOPN(1, 8);
+        else DN_TOPN(1, 16);
+    }
+#undef DN_TOPN
+    return hipGetLastError();
+}
+
+}  // namespace donerf

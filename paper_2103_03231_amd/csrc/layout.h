@@ -1,0 +1,134 @@
+// layout.h - register and memory layouts shared by the host packer and the
+// gfx950 kernels.  Host and device both include it; nothing here touches HIP.
+//
+// Networks run in the transposed form Y^T = W X^T: weights are the MFMA A
+// operand (rows = output units), activations the B operand (columns = rays or
+// samples).  A "fragment" is the A operand of one MFMA step for 32 output rows:
+//   bf16: v_mfma_f32_32x32x16_bf16, 32 rows x 16 K; lane l holds row l%32 and
+//         K slots 8*(l/32) + e, e = 0..7 (16 bytes)
+//   fp32: four v_mfma_f32_32x32x2_f32, 32 rows x 8 K; lane l holds row l%32,
+//         sub-step e = 0..3 reads K slot 2*e + l/32 (16 bytes)
+// Each fragment is stored as 64 lanes x 16 bytes = 1 KiB, so one
+// ds_read_b128 per lane fetches it without bank conflicts.
+//
+// Chaining.  The fp32 accumulator of a 32x32 MFMA block holds, on lane l
+// with g = l/32, register i = 0..15 for row 8*(i/4) + 4*g + i%4 of the block
+// and column l%32.  After bias, ReLU and (bf16) rounding those registers are
+// used in place as the next layer's B operand.  The next layer's weight
+// columns are permuted accordingly (chained_row), which is a relabelling of
+// the hidden units and leaves the network's function unchanged.
+#pragma once
+
+#if defined(__HIPCC__)
+#define DN_HD __host__ __device__
+#else
+#define DN_HD
+#endif
+
+namespace donerf {
+
+constexpr int kHidden = 256;
+constexpr int kDIn = 90;      // encode(unified origin / d_max, 10) + encode(dir, 4)
+constexpr int kSIn = 63;      // encode(warped sample, 10)
+constexpr int kSkip = 27;     // encode(dir, 4) into the last shading layer
+constexpr int kSOut = 4;      // r, g, b, sigma
+constexpr int kFragBytes = 1024;
+constexpr int kChunkFrags = 32;                 // fragments per streamed chunk
+constexpr int kChunkBytes = kChunkFrags * kFragBytes;
+constexpr int kRing = 3;                        // LDS chunk slots
+constexpr int kWaves = 4;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kMaxPosesPerLaunch = 32;
+constexpr int kRbPerPass = 2;                   // 32-row blocks per accumulator pass
+
+// Elements per lane per fragment and K per fragment.
+DN_HD constexpr int elems(bool bf16) { return bf16 ? 8 : 4; }
+DN_HD constexpr int kper(bool bf16) { return bf16 ? 16 : 8; }
+// K slot within a fragment of element e on lane group g.
+DN_HD constexpr int kslot(bool bf16, int g, int e) { return bf16 ? 8 * g + e : 2 * e + g; }
+// Number of K steps for a padded K.
+DN_HD constexpr int ksteps(bool bf16, int kpad) { return kpad / kper(bf16); }
+
+// Hidden unit (logical row of the previous layer) that feeds K step ks,
+// lane group g, element e when the previous layer's accumulators are chained.
+DN_HD constexpr int chained_row(bool bf16, int ks, int g, int e) {
+    // K steps per 32-row block: 2 (bf16) or 4 (fp32)
+    return 32 * (ks / (16 / elems(bf16))) +
+           8 * (((ks % (16 / elems(bf16))) * elems(bf16) + e) / 4) + 4 * g +
+           (((ks % (16 / elems(bf16))) * elems(bf16) + e) % 4);
+}
+
+// Per-lane feature slots.  Each column's features are split between lane
+// groups g = 0 and 1 (lanes l and l+32 serve the same ray); lane slot s of
+// group g sits at K step s / elems, element s % elems.  The maps give the
+// index of the feature in the weight blob's input order, or -1 for padding.
+// Frequencies alternate between the groups (k = 2t + g) so that both groups
+// run the same instruction stream.
+//
+// Depth network input (90 features, 96 slots, 48 per group):
+//   s in [0,30)  : position sin/cos at frequency 2t+g, t = s/6
+//   s in [30,42) : direction sin/cos at frequency 2t+g, t = (s-30)/6
+//   s in [42,45) : identity, position (g = 0) or direction (g = 1)
+//   s in [45,48) : zero
+DN_HD constexpr int d_feature(int g, int s) {
+    return s < 30 ? 3 + 6 * (2 * (s / 6) + g) + s % 6
+         : s < 42 ? 63 + 3 + 6 * (2 * ((s - 30) / 6) + g) + (s - 30) % 6
+         : s < 45 ? (g == 0 ? s - 42 : 63 + s - 42)
+         : -1;
+}
+constexpr int kDSlots = 48;
+constexpr int kDKPad = 96;
+
+// Shading network input (63 features, 64 slots, 32 per group):
+//   s in [0,30) : sin/cos at frequency 2t+g
+//   s == 30     : x (g = 0) or z (g = 1);  s == 31 : y (g = 0) or zero
+DN_HD constexpr int s_feature(int g, int s) {
+    return s < 30 ? 3 + 6 * (2 * (s / 6) + g) + s % 6
+         : s == 30 ? (g == 0 ? 0 : 2)
+         : (g == 0 ? 1 : -1);
+}
+constexpr int kSSlots = 32;
+constexpr int kSKPad = 64;
+
+// Direction skip into the last shading layer (27 features, 32 slots):
+//   s in [0,12) : sin/cos at frequency 2t+g;  s in [12,15): identity (g = 0)
+DN_HD constexpr int skip_feature(int g, int s) {
+    return s < 12 ? 3 + 6 * (2 * (s / 6) + g) + s % 6
+         : s < 15 ? (g == 0 ? s - 12 : -1)
+         : -1;
+}
+constexpr int kSkipSlots = 16;
+constexpr int kSkipKPad = 32;
+
+// Layer roles in the streamed weight sequence.
+enum LayerKind { kDFirst = 0, kHiddenL = 1, kDHead = 2, kSFirst = 3, kSHead = 4 };
+
+struct LayerGeom {
+    int out_rows;   // logical output units
+    int in_cols;    // logical inputs (blob layout)
+    int kpad;       // padded K consumed by the kernel
+    int rb;         // 32-row output blocks
+    int rbp;        // row blocks per accumulator pass
+};
+
+DN_HD constexpr LayerGeom layer_geom(int kind, int n_bins) {
+    return kind == kDFirst  ? LayerGeom{kHidden, kDIn, kDKPad, 8, kRbPerPass}
+         : kind == kHiddenL ? LayerGeom{kHidden, kHidden, kHidden, 8, kRbPerPass}
+         : kind == kDHead   ? LayerGeom{n_bins, kHidden, kHidden, n_bins / 32, kRbPerPass}
+         : kind == kSFirst  ? LayerGeom{kHidden, kSIn, kSKPad, 8, kRbPerPass}
+         :                    LayerGeom{kSOut, kHidden + kSkip, kHidden + kSkipKPad, 1, 1};
+}
+
+// Fragments a layer streams (before padding to whole chunks).
+DN_HD constexpr int layer_frags(bool bf16, int kind, int n_bins) {
+    return layer_geom(kind, n_bins).rb * ksteps(bf16, layer_geom(kind, n_bins).kpad);
+}
+DN_HD constexpr int layer_chunks(bool bf16, int kind, int n_bins) {
+    return (layer_frags(bf16, kind, n_bins) + kChunkFrags - 1) / kChunkFrags;
+}
+
+// Bias table: every layer's bias padded to 32 * rb floats, depth layers
+// then shading layers.
+DN_HD constexpr int bias_len(int kind, int n_bins) { return 32 * layer_geom(kind, n_bins).rb; }
+
+}  // namespace donerf

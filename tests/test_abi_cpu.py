@@ -1,0 +1,99 @@
+"""The C ABI without a GPU: the library loads, exports every function the
+header declares, and reports argument errors before touching a device."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2103_03231_amd import binding as b
+from paper_2103_03231_amd import inputs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "donerf.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(donerf_\w+)\s*\(", src)))
+
+
+def test_header_declarations_are_exported():
+    names = _declared()
+    assert set(names) == set(b.EXPORTS)
+    L = b.lib()
+    for n in names:
+        assert hasattr(L, n), n
+
+
+@pytest.mark.parametrize("B", [64, 128, 192, 256])
+def test_weight_count_matches_blob(B):
+    assert b.donerf_weight_count(B) == inputs.n_weights(B) == inputs.make_weights(B, 0).size
+    assert b.donerf_weight_count(0) == 0
+
+
+def test_status_strings():
+    for s in (0, -1, -2, -3, -4, -5, -6, -7):
+        assert b.donerf_status_str(s) and b.donerf_status_str(s) != "unknown status"
+    assert b.donerf_status_str(-99) == "unknown status"
+
+
+W128 = inputs.make_weights(128, 0)
+
+
+@pytest.mark.parametrize("kw,status", [
+    ({"near": 0.0}, b.E_INVALID_ARG),
+    ({"near": 5.0, "far": 5.0}, b.E_INVALID_ARG),
+    ({"fov_x_deg": 180.0}, b.E_INVALID_ARG),
+    ({"radius": -1.0}, b.E_INVALID_ARG),
+    ({"n_max": 0}, b.E_INVALID_ARG),
+    ({"n_max": 17}, b.E_INVALID_ARG),
+    ({"precision": 7}, b.E_INVALID_ARG),
+    ({"select": 3}, b.E_INVALID_ARG),
+    ({"far": float("inf")}, b.E_NONFINITE),
+    ({"centre": (0.0, float("nan"), 0.0)}, b.E_NONFINITE),
+    ({"n_bins": 100}, b.E_UNSUPPORTED),
+    ({"n_bins": 32}, b.E_UNSUPPORTED),
+])
+def test_create_rejects_bad_config(kw, status):
+    with pytest.raises(b.DonerfError) as e:
+        b.donerf_create(b.Config(**kw), W128)
+    assert e.value.status == status
+    assert b.donerf_last_error()
+
+
+def test_create_rejects_bad_weights():
+    with pytest.raises(b.DonerfError) as e:
+        b.donerf_create(b.Config(), W128[:-1])
+    assert e.value.status == b.E_SIZE
+    w = W128.copy()
+    w[12345] = np.inf
+    with pytest.raises(b.DonerfError) as e:
+        b.donerf_create(b.Config(), w)
+    assert e.value.status == b.E_NONFINITE
+    with pytest.raises(b.DonerfError) as e:
+        b.donerf_create(b.Config(), None)
+    assert e.value.status == b.E_INVALID_ARG
+
+
+def test_calls_on_null_handle():
+    poses = inputs.make_poses([0])
+    for fn in (lambda: b.donerf_render(None, poses, 1, 4, 4, 4, 1),
+               lambda: b.donerf_render_debug(None, poses, 1, 4, 4, 4, 1),
+               lambda: b.donerf_debug_topn(None, 1, 4, 4, 1),
+               lambda: b.donerf_debug_bins(None, 128),
+               lambda: b.donerf_set_stream(None, 0)):
+        with pytest.raises(b.DonerfError) as e:
+            fn()
+        assert e.value.status == b.E_INVALID_ARG
+    b.donerf_destroy(None)
+
+
+def test_create_without_gpu_reports_device_error():
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    with pytest.raises(b.DonerfError) as e:
+        b.donerf_create(b.Config(), W128)
+    assert e.value.status == b.E_DEVICE

@@ -1,0 +1,244 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Selection is compared bit for bit on identical scores.  End to end, rays
+whose selected classes differ from the oracle's (near-tied scores, "flips")
+are re-rendered by the oracle with the GPU's selection forced; RGB must then
+agree within 1e-4 (fp32 path, against the fp64 oracle) or 2e-2 (bf16 path,
+against the bf16-rounding oracle) on every ray.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import donerf_oracle as O
+from paper_2103_03231_amd import binding as b
+from paper_2103_03231_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"fp32": 1e-4, "bf16": 2e-2}
+PREC = {"fp32": b.FP32, "bf16": b.BF16}
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def renderer(precision, n_bins=128, n_max=4, fov=60.0, select=b.SELECT_TOPN, seed=0):
+    w = inputs.make_weights(n_bins, seed)
+    cfg = b.Config(n_bins=n_bins, n_max=n_max, precision=PREC[precision], fov_x_deg=fov, select=select)
+    return b.Renderer(cfg, w), w
+
+
+def gpu_render(r, poses, H, W, N):
+    out = r.render(poses, H, W, N, depth=True, debug=True)
+    torch.cuda.synchronize()
+    return {k: v.cpu().numpy() for k, v in out.items()}
+
+
+def check_against_oracle(g, w, poses, H, W, N, precision, n_bins=128, fov=60.0, subset=None,
+                         max_flip_frac=0.0, label=""):
+    gb = g["bins"].reshape(-1, N)
+    rgb = g["rgb"].reshape(-1, 3)
+    depth = g["depth"].reshape(-1)
+    scores = g["scores"].reshape(-1, n_bins)
+    if subset is not None:
+        gb, rgb, depth, scores = gb[subset], rgb[subset], depth[subset], scores[subset]
+    ora = O.render(w, poses, H, W, N, n_bins=n_bins, fov_x_deg=fov, precision=precision,
+                   forced_bins=gb, ray_subset=subset)
+    natural = O.topn(ora["logits"].astype(np.float32), N)
+    flips = np.any(natural != gb, axis=1)
+    err = np.abs(rgb - ora["rgb"]).max()
+    derr = np.abs(depth - ora["depth"]).max()
+    serr = np.abs(scores - ora["logits"]).max()
+    log(f"[{label}] rays={len(gb)} flips={flips.sum()} rgb_maxabs={err:.3e} depth_maxabs={derr:.3e} "
+        f"score_maxabs={serr:.3e}")
+    assert np.all(np.isfinite(rgb)) and np.all((rgb >= 0) & (rgb <= 1))
+    assert flips.mean() <= max_flip_frac, flips.mean()
+    assert err <= TOL[precision], err
+    # depth = sum w t with t <= d_max: the same relative tolerance
+    assert derr <= TOL[precision] * 10.0, derr
+    return err, flips
+
+
+# ------------------------------------------------------------------ depth classes
+
+@pytest.mark.parametrize("B", [64, 128, 256])
+def test_bin_table_bit_exact(B):
+    r, _ = renderer("bf16", n_bins=B)
+    bounds, centres, widths = b.donerf_debug_bins(r.h, B)
+    ob, oc, ow = O.bin_table(0.1, 10.0, B)
+    assert np.array_equal(bounds, ob) and np.array_equal(centres, oc) and np.array_equal(widths, ow)
+    r.close()
+
+
+# ------------------------------------------------------------------ selection
+
+@pytest.mark.parametrize("precision", ["fp32", "bf16"])
+@pytest.mark.parametrize("B", [64, 128, 192, 256])
+def test_topn_bit_exact(precision, B):
+    r, _ = renderer(precision, n_bins=B, n_max=16)
+    for mode in ("normal", "ties", "const"):
+        lg = inputs.random_logits(3001, B, seed=B, mode=mode)
+        dev = torch.from_numpy(lg).cuda()
+        for N in (1, 3, 4, 5, 8, 16):
+            out = torch.empty((lg.shape[0], N), dtype=torch.int32, device="cuda")
+            b.donerf_debug_topn(r.h, dev.data_ptr(), lg.shape[0], N, out.data_ptr())
+            torch.cuda.synchronize()
+            got = out.cpu().numpy()
+            ref = O.topn(lg, N)
+            bad = np.nonzero(np.any(got != ref, axis=1))[0]
+            assert len(bad) == 0, (mode, N, bad[:5], got[bad[:2]], ref[bad[:2]])
+    r.close()
+
+
+def test_topn_million_rows():
+    r, _ = renderer("bf16", n_bins=128, n_max=4)
+    lg = inputs.random_logits(1_000_000, 128, seed=99)
+    dev = torch.from_numpy(lg).cuda()
+    out = torch.empty((lg.shape[0], 4), dtype=torch.int32, device="cuda")
+    b.donerf_debug_topn(r.h, dev.data_ptr(), lg.shape[0], 4, out.data_ptr())
+    torch.cuda.synchronize()
+    assert np.array_equal(out.cpu().numpy(), O.topn(lg, 4))
+    r.close()
+
+
+# ------------------------------------------------------------------ end to end
+
+def test_tiny32_fp32_against_fp64_oracle():
+    """32x32 rays, pose seed 0, B=128, N=4, fp32."""
+    r, w = renderer("fp32")
+    poses = inputs.make_poses([0])
+    g = gpu_render(r, poses, 32, 32, 4)
+    check_against_oracle(g, w, poses, 32, 32, 4, "fp32", label="tiny32 fp32")
+    r.close()
+
+
+def test_bf16_small_frames_against_bf16_oracle():
+    r, w = renderer("bf16")
+    poses = inputs.make_poses([1, 2])
+    g = gpu_render(r, poses, 40, 48, 4)
+    check_against_oracle(g, w, poses, 40, 48, 4, "bf16", max_flip_frac=0.02, label="bf16 2x40x48")
+    r.close()
+
+
+@pytest.mark.parametrize("precision", ["fp32", "bf16"])
+@pytest.mark.parametrize("N,B,H,W,P", [
+    (1, 128, 17, 23, 1),
+    (2, 128, 37, 29, 1),      # ragged tail
+    (3, 64, 16, 16, 2),       # N below the list capacity
+    (8, 256, 16, 24, 1),
+    (16, 256, 12, 20, 1),
+    (4, 192, 3, 5, 35),       # more poses than one launch holds
+])
+def test_variants(precision, N, B, H, W, P):
+    r, w = renderer(precision, n_bins=B, n_max=max(N, 4))
+    poses = inputs.make_poses(list(range(P)))
+    g = gpu_render(r, poses, H, W, N)
+    check_against_oracle(g, w, poses, H, W, N, precision, n_bins=B,
+                         max_flip_frac=0.0 if precision == "fp32" else 0.03,
+                         label=f"{precision} N={N} B={B} {P}x{H}x{W}")
+    r.close()
+
+
+def test_fov90_and_softmax_scores():
+    rt, w = renderer("fp32", fov=90.0)
+    rs, _ = renderer("fp32", fov=90.0, select=b.SELECT_TOPN_SOFTMAX)
+    poses = inputs.make_poses([3])
+    gt = gpu_render(rt, poses, 24, 40, 4)
+    gs = gpu_render(rs, poses, 24, 40, 4)
+    assert np.array_equal(gt["bins"], gs["bins"])
+    assert np.array_equal(gt["rgb"], gs["rgb"])
+    p = gs["scores"].reshape(-1, 128)
+    np.testing.assert_allclose(p.sum(1), 1.0, atol=1e-5)
+    ref = O.softmax_fp32(gt["scores"].reshape(-1, 128))
+    np.testing.assert_allclose(p, ref, rtol=1e-5, atol=1e-8)
+    check_against_oracle(gt, w, poses, 24, 40, 4, "fp32", fov=90.0, label="fov90")
+    rt.close()
+    rs.close()
+
+
+def test_deterministic_and_plain_render_matches_debug():
+    r, _ = renderer("bf16")
+    poses = inputs.make_poses([4, 5])
+    a = gpu_render(r, poses, 33, 31, 4)
+    c = gpu_render(r, poses, 33, 31, 4)
+    for k in a:
+        assert np.array_equal(a[k], c[k]), k
+    plain = r.render(poses, 33, 31, 4, depth=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(plain["rgb"].cpu().numpy(), a["rgb"])
+    assert np.array_equal(plain["depth"].cpu().numpy(), a["depth"])
+    r.close()
+
+
+def test_render_rejects_bad_sample_count():
+    r, _ = renderer("bf16", n_max=4)
+    poses = inputs.make_poses([0])
+    out = r.alloc(1, 8, 8, 4)
+    for N in (0, 5):
+        with pytest.raises(b.DonerfError) as e:
+            b.donerf_render(r.h, poses, 1, 8, 8, N, out["rgb"].data_ptr())
+        assert e.value.status == b.E_INVALID_ARG
+    bad = poses.copy()
+    bad[0, 1, 3] = np.nan
+    with pytest.raises(b.DonerfError) as e:
+        b.donerf_render(r.h, bad, 1, 8, 8, 4, out["rgb"].data_ptr())
+    assert e.value.status == b.E_NONFINITE
+    r.close()
+
+
+# ------------------------------------------------------------------ full-size workloads, sampled
+
+def _sampled(workload, n_sample, seed=0):
+    wl = inputs.WORKLOADS[workload]
+    r, w = renderer(wl.precision, n_bins=wl.n_bins, n_max=wl.N, fov=wl.fov_deg,
+                    select=b.SELECT_TOPN_SOFTMAX if wl.select == "topn_softmax" else b.SELECT_TOPN)
+    poses = wl.poses()
+    if wl.name.startswith("stereo"):
+        poses = poses[:2]            # one stereo pair of the 60-pose sequence
+    P = len(poses)
+    out = r.alloc(P, wl.H, wl.W, wl.N, depth=True)
+    out["bins"] = torch.empty((P, wl.H, wl.W, wl.N), dtype=torch.int32, device="cuda")
+    log(f"[{workload}] rendering {P}x{wl.H}x{wl.W} N={wl.N} B={wl.n_bins}")
+    r.render_into(poses, wl.H, wl.W, wl.N, out, debug=True)
+    torch.cuda.synchronize()
+    rgb = out["rgb"].reshape(-1, 3)
+    assert bool(torch.isfinite(rgb).all()) and float(rgb.min()) >= 0 and float(rgb.max()) <= 1
+    rng = np.random.default_rng(seed)
+    total = P * wl.H * wl.W
+    subset = np.unique(np.concatenate([rng.integers(0, total, n_sample), [0, total - 1]]))
+    sub = torch.from_numpy(subset).cuda()
+    g = {"rgb": out["rgb"].reshape(-1, 3)[sub].cpu().numpy(),
+         "depth": out["depth"].reshape(-1)[sub].cpu().numpy(),
+         "bins": out["bins"].reshape(-1, wl.N)[sub].cpu().numpy()}
+    gb = g["bins"]
+    ora = O.render(w, poses, wl.H, wl.W, wl.N, n_bins=wl.n_bins, fov_x_deg=wl.fov_deg,
+                   precision=wl.precision, forced_bins=gb, ray_subset=subset)
+    flips = np.any(O.topn(ora["logits"].astype(np.float32), wl.N) != gb, axis=1)
+    err = np.abs(g["rgb"] - ora["rgb"]).max()
+    derr = np.abs(g["depth"] - ora["depth"]).max()
+    log(f"[{workload}] sampled={len(subset)} flips={flips.sum()} rgb_maxabs={err:.3e} depth_maxabs={derr:.3e}")
+    assert err <= TOL[wl.precision]
+    assert derr <= 10 * TOL[wl.precision]
+    assert flips.mean() <= 0.03
+    r.close()
+
+
+def test_frame400_n4_bf16_sampled():
+    _sampled("frame400_n4_bf16", 3000)
+
+
+def test_frame800_n8_depth_bf16_sampled():
+    _sampled("frame800_n8_depth_bf16", 1500)
+
+
+def test_hd1080_n4_softmax_bf16_sampled():
+    _sampled("hd1080_n4_softmax_bf16", 1500)
+
+
+def test_stereo_n16_b256_bf16_sampled():
+    _sampled("stereo1440x1600_n16_b256_bf16", 800)
