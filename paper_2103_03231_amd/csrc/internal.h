@@ -31,8 +31,23 @@ struct RenderArgs {
     float poses[kMaxPosesPerLaunch][12];
 };
 
+// Launch shape of the bf16 render kernel: 32-ray column blocks per wave and
+// waves per workgroup, and waves per SIMD the register budget is sized for.
+#ifndef DONERF_BF16_CB
+#define DONERF_BF16_CB 1
+#endif
+#ifndef DONERF_BF16_NW
+#define DONERF_BF16_NW 8
+#endif
+#ifndef DONERF_BF16_OCC
+#define DONERF_BF16_OCC 2
+#endif
+constexpr int kBf16CB = DONERF_BF16_CB;
+constexpr int kBf16NW = DONERF_BF16_NW;
+constexpr int kBf16Occ = DONERF_BF16_OCC;
+
 // Rays handled by one workgroup.
-inline int rays_per_block(bool bf16) { return kWaves * 32 * (bf16 ? 2 : 1); }
+inline int rays_per_block(bool bf16) { return bf16 ? kBf16NW * 32 * kBf16CB : 4 * 32; }
 
 hipError_t launch_render(bool bf16, int ncap, const RenderArgs& a, hipStream_t stream);
 hipError_t launch_softmax_rows(float* scores, uint32_t rows, int B, hipStream_t stream);

@@ -56,7 +56,6 @@ struct Prec;
 template <>
 struct Prec<true> {
     static constexpr int E = 8;      // K elements per lane per fragment
-    static constexpr int CB = 2;     // 32-column blocks per wave
     static constexpr int KSPB = 2;   // K steps produced per 32-row block
     __device__ static __forceinline__ f32x16 mma(u32x4 a, u32x4 b, f32x16 c) {
         return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
@@ -71,7 +70,6 @@ struct Prec<true> {
 template <>
 struct Prec<false> {
     static constexpr int E = 4;
-    static constexpr int CB = 1;
     static constexpr int KSPB = 4;
     __device__ static __forceinline__ f32x16 mma(u32x4 a, u32x4 b, f32x16 c) {
         c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
@@ -95,58 +93,66 @@ __device__ __forceinline__ void lds_barrier() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-constexpr int kChunkVec = kChunkBytes / 16;           // u32x4 per chunk
-constexpr int kStagePerThread = kChunkVec / kThreads;  // u32x4 each thread moves per chunk
+constexpr int kChunkVec = kChunkBytes / 16;  // u32x4 per chunk
+constexpr int kFragAhead = 2;                 // LDS fragment reads in flight
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
+template <int VM>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(VM >= 0 && VM < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4) | (15 << 8));
+}
 
 // The workgroup consumes one logical sequence of chunks: every depth-network
-// chunk, then the shading-network chunks once per sample.  Chunk c+1 is
-// copied into LDS while chunk c is consumed and chunk c+2 is in flight from
-// L2 in registers; one barrier per chunk.
+// chunk, then the shading-network chunks once per sample.  Chunks travel
+// from L2 straight into LDS (global_load_lds, 16 bytes per lane), kRing - 1
+// chunks ahead of use, in a ring of kRing slots.  Each wave copies
+// kChunkFrags / NW fragments of every chunk; advancing to chunk c waits for
+// the wave's own copies of c (later chunks stay in flight) and then
+// barriers, which both publishes c and retires every reader of chunk c-1,
+// whose slot the copy of chunk c + kRing - 1 then reuses.  The copy count per
+// step is constant (the stream index is clamped past its end) so the counter
+// arithmetic holds at the tail.
+template <int NW>
 struct WeightStream {
+    static constexpr int FPW = kChunkFrags / NW;  // fragments each wave copies per chunk
+    static constexpr int AHEAD = kRing - 1;
+    static_assert(kChunkFrags % NW == 0, "chunk split");
     const u32x4* dsrc;
     const u32x4* ssrc;
     u32x4* ring;
     int nd, ns, total;
-    int c;      // chunk being consumed
-    int slot;   // its LDS slot
-    int tid;
-    u32x4 stage[kStagePerThread];
+    int c;       // chunk being consumed
+    int slot;    // its LDS slot
+    int lane, wave;
 
     __device__ __forceinline__ const u32x4* src(int k) const {
+        k = k < total ? k : total - 1;
         return k < nd ? dsrc + (size_t)k * kChunkVec : ssrc + (size_t)((k - nd) % ns) * kChunkVec;
     }
-    __device__ __forceinline__ void load(int k) {
-        if (k < total) {
-            const u32x4* p = src(k) + tid;
+    __device__ __forceinline__ void issue(int k, int dst_slot) {
+        const u32x4* sp = src(k) + wave * FPW * 64 + lane;
+        u32x4* dp = ring + dst_slot * kChunkVec + wave * FPW * 64;
 #pragma unroll
-            for (int i = 0; i < kStagePerThread; ++i) stage[i] = p[i * kThreads];
-        }
-    }
-    __device__ __forceinline__ void store(int k) {
-        if (k < total) {
-            u32x4* q = ring + (k % kRing) * kChunkVec + tid;
-#pragma unroll
-            for (int i = 0; i < kStagePerThread; ++i) q[i * kThreads] = stage[i];
-        }
+        for (int i = 0; i < FPW; ++i)
+            __builtin_amdgcn_global_load_lds(sp + i * 64, dp + i * 64, 16, 0, 0);
     }
     __device__ __forceinline__ void start() {
         c = -1;
         slot = kRing - 1;
-        load(0);
-        store(0);
-        load(1);
+#pragma unroll
+        for (int k = 0; k < AHEAD; ++k) issue(k, k);
     }
-    // Advance to the next chunk: publish chunk c+1, barrier, prefetch c+2.
     __device__ __forceinline__ void next() {
         ++c;
         slot = slot == kRing - 1 ? 0 : slot + 1;
-        store(c + 1);
+        wait_vmcnt<FPW * (AHEAD - 1)>();
         lds_barrier();
-        load(c + 2);
+        // the slot of chunk c - 1, i.e. the one before c's in ring order
+        issue(c + AHEAD, slot == 0 ? kRing - 1 : slot - 1);
     }
-    __device__ __forceinline__ u32x4 frag(int i, int lane) const {
-        return ring[slot * kChunkVec + i * 64 + lane];
-    }
+    __device__ __forceinline__ void finish() { wait_vmcnt<0>(); }
+    __device__ __forceinline__ u32x4 frag(int i) const { return ring[slot * kChunkVec + i * 64 + lane]; }
 };
 
 // ------------------------------------------------------------------ MFMA layers
@@ -169,52 +175,111 @@ __device__ __forceinline__ f32x16 bias_frag(const float* bias, int g) {
 // One accumulator pass: RBP output row blocks x CB column blocks over KS K
 // steps.  BASE is the index of the pass's first fragment within its layer;
 // layers start on chunk boundaries, so chunk changes are known statically.
-template <bool BF16, int KS, int RBP, int BASE, class GetB, class Epi>
-__device__ __forceinline__ void run_pass(WeightStream& st, int lane, int g, const float* bias,
-                                         GetB& getB, Epi&& epi) {
+template <bool BF16, int CB, int KS, int RBP, int BASE, class WS, class GetB, class Epi>
+__device__ __forceinline__ void run_pass(WS& st, int g, const float* bias, GetB& getB, Epi&& epi) {
     using P = Prec<BF16>;
-    f32x16 acc[RBP][P::CB];
+    constexpr int NF = KS * RBP;   // fragments of the pass, in (K step, row block) order
+    constexpr int D = kFragAhead;  // LDS reads issued this many fragments ahead
+    f32x16 acc[RBP][CB];
     sfor<RBP>([&](auto R) {
         const f32x16 b = bias_frag(bias + 32 * CV(R), g);
-        sfor<P::CB>([&](auto C) { acc[CV(R)][CV(C)] = b; });
+        sfor<CB>([&](auto C) { acc[CV(R)][CV(C)] = b; });
     });
-    sfor<KS>([&](auto K) {
-        sfor<RBP>([&](auto R) {
-            constexpr int idx = BASE + CV(K) * RBP + CV(R);
+    u32x4 a[NF];
+    // Software pipeline: step s reads fragment s and multiplies fragment
+    // s - D.  The scheduling barriers keep LDS reads and MFMAs in this order
+    // (bounding the registers held by fragments in flight) while VALU and
+    // SALU work may move across them.
+    sfor<NF + D>([&](auto S) {
+        constexpr int s = CV(S);
+        if constexpr (s < NF) {
+            constexpr int idx = BASE + s;
             if constexpr (idx % kChunkFrags == 0) st.next();
-            const u32x4 a = st.frag(idx % kChunkFrags, lane);
-            sfor<P::CB>([&](auto C) {
-                acc[CV(R)][CV(C)] = P::mma(a, getB(K, C), acc[CV(R)][CV(C)]);
+            a[s] = st.frag(idx % kChunkFrags);
+        }
+        if constexpr (s >= D) {
+            constexpr int f = s - D;
+            constexpr int k = f / RBP, r = f % RBP;
+            sfor<CB>([&](auto C) {
+                acc[r][CV(C)] = P::mma(a[f], getB(std::integral_constant<int, k>{}, C), acc[r][CV(C)]);
             });
-        });
+        }
+        __builtin_amdgcn_sched_barrier(0x6);
     });
-    sfor<RBP>([&](auto R) { sfor<P::CB>([&](auto C) { epi(R, C, acc[CV(R)][CV(C)]); }); });
+    sfor<RBP>([&](auto R) { sfor<CB>([&](auto C) { epi(R, C, acc[CV(R)][CV(C)]); }); });
 }
 
 // ReLU, round, and place a 32-row accumulator block as K steps
-// [ks0, ks0 + KSPB) of the next layer's B operand.
+// [ks0, ks0 + KSPB) of the next layer's B operand.  bf16: round to nearest
+// even, then ReLU on the packed pair as a signed 16-bit max with 0 (rounding
+// preserves the sign, so this equals rounding the ReLU).
 template <bool BF16, int NK, int CB>
 __device__ __forceinline__ void emit_relu(const f32x16& acc, u32x4 (&out)[NK][CB], int ks0, int cb) {
     using P = Prec<BF16>;
-    float v[16];
+    if constexpr (BF16) {
+        typedef short i16x2 __attribute__((ext_vector_type(2)));
 #pragma unroll
-    for (int i = 0; i < 16; ++i) v[i] = fmaxf(acc[i], 0.0f);
+        for (int h = 0; h < P::KSPB; ++h) {
+            u32x4 o;
 #pragma unroll
-    for (int h = 0; h < P::KSPB; ++h) out[ks0 + h][cb] = P::pack(v + h * P::E);
+            for (int w = 0; w < 4; ++w) {
+                const i16x2 v = __builtin_bit_cast(i16x2, pack_bf16x2(acc[8 * h + 2 * w], acc[8 * h + 2 * w + 1]));
+                o[w] = __builtin_bit_cast(uint32_t, __builtin_elementwise_max(v, i16x2{0, 0}));
+            }
+            out[ks0 + h][cb] = o;
+        }
+    } else {
+        float v[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) v[i] = fmaxf(acc[i], 0.0f);
+#pragma unroll
+        for (int h = 0; h < P::KSPB; ++h) out[ks0 + h][cb] = P::pack(v + h * P::E);
+    }
 }
 
-// Fully connected ReLU layer with 256 outputs (8 row blocks).
-template <bool BF16, int KS, class GetB>
-__device__ __forceinline__ void hidden_layer(WeightStream& st, int lane, int g, const float* bias,
-                                             GetB&& getB,
-                                             u32x4 (&out)[8 * Prec<BF16>::KSPB][Prec<BF16>::CB]) {
+// Fully connected ReLU layer with 256 outputs (8 row blocks) as one software
+// pipeline over its KS * 8 fragments: passes of kRbPerPass row blocks use
+// alternating accumulator sets, so the bias/ReLU/rounding of pass p can
+// overlap the MFMAs of pass p + 1, and LDS reads run kFragAhead fragments
+// ahead across pass and chunk boundaries.
+template <bool BF16, int CB, int KS, class WS, class GetB>
+__device__ __forceinline__ void hidden_layer(WS& st, int g, const float* bias, GetB&& getB,
+                                             u32x4 (&out)[8 * Prec<BF16>::KSPB][CB]) {
     using P = Prec<BF16>;
-    sfor<8 / kRbPerPass>([&](auto PI) {
-        constexpr int p = CV(PI);
-        run_pass<BF16, KS, kRbPerPass, p * KS * kRbPerPass>(
-            st, lane, g, bias + 32 * kRbPerPass * p, getB, [&](auto R, auto C, const f32x16& acc) {
-                emit_relu<BF16>(acc, out, (p * kRbPerPass + CV(R)) * P::KSPB, CV(C));
+    constexpr int RBP = kRbPerPass;
+    constexpr int PF = KS * RBP;       // fragments per pass
+    constexpr int NF = 8 * KS;         // fragments of the layer
+    constexpr int D = kFragAhead;
+    f32x16 acc[2][RBP][CB];
+    u32x4 a[D + 1];
+    sfor<NF + D>([&](auto S) {
+        constexpr int s = CV(S);
+        if constexpr (s < NF) {
+            if constexpr (s % kChunkFrags == 0) st.next();
+            a[s % (D + 1)] = st.frag(s % kChunkFrags);
+        }
+        if constexpr (s >= D) {
+            constexpr int f = s - D;
+            constexpr int p = f / PF, w = f % PF, k = w / RBP, r = w % RBP;
+            if constexpr (w == 0) {
+                sfor<RBP>([&](auto R) {
+                    const f32x16 b = bias_frag(bias + 32 * (RBP * p + CV(R)), g);
+                    sfor<CB>([&](auto C) { acc[p & 1][CV(R)][CV(C)] = b; });
+                });
+            }
+            sfor<CB>([&](auto C) {
+                acc[p & 1][r][CV(C)] = P::mma(a[f % (D + 1)], getB(std::integral_constant<int, k>{}, C),
+                                              acc[p & 1][r][CV(C)]);
             });
+            if constexpr (w == PF - 1) {
+                sfor<RBP>([&](auto R) {
+                    sfor<CB>([&](auto C) {
+                        emit_relu<BF16>(acc[p & 1][CV(R)][CV(C)], out, (p * RBP + CV(R)) * P::KSPB, CV(C));
+                    });
+                });
+            }
+        }
+        __builtin_amdgcn_sched_barrier(0x6);
     });
 }
 
@@ -348,17 +413,34 @@ __device__ __forceinline__ void warp(const RenderArgs& a, const float (&x)[3], f
 
 // Encoding slots: T frequency pairs 2t + g (t < T) of v, written as
 // [sin x, sin y, sin z, cos x, cos y, cos z] per frequency.  The scale 2^k is
-// exact in fp32 and sincospi avoids multiplying by a rounded pi.
-template <int T>
+// exact in fp32 and sincospi avoids multiplying by a rounded pi.  With EXACT
+// false (bf16 networks) only frequencies 2t + g with t % 3 == 0 are evaluated
+// directly; the others follow by two double-angle steps each,
+// sin 2a = 2 sin a cos a and cos 2a = (cos a - sin a)(cos a + sin a), whose
+// error (at most four steps from a direct value, about 16 fp32 ulp) stays far
+// below the bf16 rounding the features then undergo.
+#ifndef DONERF_PE_EXACT
+#define DONERF_PE_EXACT 0
+#endif
+template <int T, bool EXACT>
 __device__ __forceinline__ void fourier(const float (&v)[3], int g, float* f) {
     const float gs = g ? 2.0f : 1.0f;
 #pragma unroll
-    for (int t = 0; t < T; ++t) {
-        const float sc = (float)(1u << (2 * t)) * gs;
+    for (int c = 0; c < 3; ++c) {
+        float s = 0.0f, co = 1.0f;
 #pragma unroll
-        for (int c = 0; c < 3; ++c) {
-            float s, co;
-            sincospif(v[c] * sc, &s, &co);
+        for (int t = 0; t < T; ++t) {
+            if (EXACT || DONERF_PE_EXACT || t % 3 == 0) {
+                const float sc = (float)(1u << (2 * t)) * gs;
+                sincospif(v[c] * sc, &s, &co);
+            } else {
+#pragma unroll
+                for (int d = 0; d < 2; ++d) {
+                    const float s2 = (s + s) * co;
+                    co = (co - s) * (co + s);
+                    s = s2;
+                }
+            }
             f[6 * t + c] = s;
             f[6 * t + 3 + c] = co;
         }
@@ -369,16 +451,19 @@ __device__ __forceinline__ void fourier(const float (&v)[3], int g, float* f) {
 
 constexpr int kBiasMax = 7 * 256 + 256 + 7 * 256 + 32;
 
-template <bool BF16, int NCAP>
-__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+// BF16: network precision.  CB: 32-ray column blocks per wave.  NW: waves per
+// workgroup.  OCC: waves per SIMD the register budget is sized for (with
+// OCC * 4 > NW several workgroups share a CU).  NCAP: capacity of the top-N
+// list.
+template <bool BF16, int CB, int NW, int OCC, int NCAP>
+__global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(OCC, OCC)))
 render_kernel(const RenderArgs a) {
     using P = Prec<BF16>;
-    constexpr int CB = P::CB;
     constexpr int E = P::E;
-    constexpr int KS_D0 = kDKPad / (2 * E);   // 6 | 12
-    constexpr int KS_H = kHidden / (2 * E);   // 16 | 32
-    constexpr int KS_S0 = kSKPad / (2 * E);   // 4 | 8
-    constexpr int KS_SK = kSkipKPad / (2 * E);// 2 | 4
+    constexpr int KS_D0 = kDKPad / (2 * E);    // 6 | 12
+    constexpr int KS_H = kHidden / (2 * E);    // 16 | 32
+    constexpr int KS_S0 = kSKPad / (2 * E);    // 4 | 8
+    constexpr int KS_SK = kSkipKPad / (2 * E); // 2 | 4
 
     __shared__ u32x4 ring[kRing * kChunkVec];
     __shared__ float bias_s[kBiasMax];
@@ -390,21 +475,22 @@ render_kernel(const RenderArgs a) {
     const int g = lane >> 5;
     const int col = lane & 31;
 
-    for (int k = tid; k < a.bias_len; k += kThreads) bias_s[k] = a.bias[k];
-    for (int k = tid; k < 2 * a.B; k += kThreads) bins_s[k] = a.bins[k];
+    for (int k = tid; k < a.bias_len; k += 64 * NW) bias_s[k] = a.bias[k];
+    for (int k = tid; k < 2 * a.B; k += 64 * NW) bins_s[k] = a.bins[k];
 
-    WeightStream st;
+    WeightStream<NW> st;
     st.dsrc = reinterpret_cast<const u32x4*>(a.d_frags);
     st.ssrc = reinterpret_cast<const u32x4*>(a.s_frags);
     st.ring = ring;
     st.nd = a.n_d_chunks;
     st.ns = a.n_s_chunks;
     st.total = a.n_d_chunks + a.N * a.n_s_chunks;
-    st.tid = tid;
+    st.lane = lane;
+    st.wave = wave;
     st.start();
 
     // ---- rays of this wave: column col of block cb
-    const uint32_t ray0 = ((uint32_t)blockIdx.x * kWaves + wave) * (32 * CB);
+    const uint32_t ray0 = ((uint32_t)blockIdx.x * NW + wave) * (32 * CB);
     uint32_t rid[CB];
     bool valid[CB];
     Ray ray[CB];
@@ -422,14 +508,16 @@ render_kernel(const RenderArgs a) {
         v[1] = (ou[1] - a.cy) / a.dmax;
         v[2] = (ou[2] - a.cz) / a.dmax;
         float f[kDSlots];
-        fourier<5>(v, g, f);
-        fourier<2>(ray[cb].r, g, f + 30);
+        fourier<5, !BF16>(v, g, f);
+        fourier<2, !BF16>(ray[cb].r, g, f + 30);
         f[42] = g ? ray[cb].r[0] : v[0];
         f[43] = g ? ray[cb].r[1] : v[1];
         f[44] = g ? ray[cb].r[2] : v[2];
         f[45] = f[46] = f[47] = 0.0f;
 #pragma unroll
         for (int ks = 0; ks < KS_D0; ++ks) din[ks][cb] = P::pack(f + E * ks);
+        // the direction skip of the last shading layer: the same direction
+        // encoding plus the identity
         float fs[kSkipSlots];
 #pragma unroll
         for (int k = 0; k < 12; ++k) fs[k] = f[30 + k];
@@ -440,37 +528,47 @@ render_kernel(const RenderArgs a) {
 #pragma unroll
         for (int ks = 0; ks < KS_SK; ++ks) skip[ks][cb] = P::pack(fs + E * ks);
     }
-    lds_barrier();  // bias_s / bins_s visible (the stream also barriers)
+    lds_barrier();  // bias_s and bins_s visible
 
     // ---- depth-oracle network
     u32x4 h0[KS_H][CB], h1[KS_H][CB];
     {
         auto gin = [&](auto K, auto C) { return din[CV(K)][CV(C)]; };
-        hidden_layer<BF16, KS_D0>(st, lane, g, bias_s, gin, h0);
+        hidden_layer<BF16, CB, KS_D0>(st, g, bias_s, gin, h0);
     }
     auto g0 = [&](auto K, auto C) { return h0[CV(K)][CV(C)]; };
     auto g1 = [&](auto K, auto C) { return h1[CV(K)][CV(C)]; };
     for (int l = 0; l < 3; ++l) {
-        hidden_layer<BF16, KS_H>(st, lane, g, bias_s + 256 * (1 + 2 * l), g0, h1);
-        hidden_layer<BF16, KS_H>(st, lane, g, bias_s + 256 * (2 + 2 * l), g1, h0);
+        hidden_layer<BF16, CB, KS_H>(st, g, bias_s + 256 * (1 + 2 * l), g0, h1);
+        hidden_layer<BF16, CB, KS_H>(st, g, bias_s + 256 * (2 + 2 * l), g1, h0);
     }
     TopList<NCAP> top[CB];
-#pragma unroll
-    for (int cb = 0; cb < CB; ++cb) top[cb].init();
+    sfor<CB>([&](auto C) { top[CV(C)].init(); });
+    // Head of the depth network: B / 64 passes of 64 classes.  PPC passes
+    // share one chunk, so the loop steps a chunk at a time.
     const int npass = a.B / (32 * kRbPerPass);
-    for (int p = 0; p < npass; ++p) {
-        run_pass<BF16, KS_H, kRbPerPass, 0>(
-            st, lane, g, bias_s + 7 * 256 + 64 * p, g0, [&](auto R, auto C, const f32x16& acc) {
-                const int rowb = 64 * p + 32 * CV(R) + 4 * g;
+    constexpr int PASS_FRAGS = KS_H * kRbPerPass;
+    constexpr int PPC = PASS_FRAGS >= kChunkFrags ? 1 : kChunkFrags / PASS_FRAGS;
+    for (int p0 = 0; p0 < npass; p0 += PPC) {
+        sfor<PPC>([&](auto Q) {
+            constexpr int q = CV(Q);
+            const int p = p0 + q;
+            if (p < npass) {
+                run_pass<BF16, CB, KS_H, kRbPerPass, q * PASS_FRAGS>(
+                    st, g, bias_s + 7 * 256 + 64 * p, g0, [&](auto R, auto C, const f32x16& acc) {
+                        const int rowb = 64 * p + 32 * CV(R) + 4 * g;
 #pragma unroll
-                for (int i = 0; i < 16; ++i) top[CV(C)].push_ascending(acc[i], rowb + 8 * (i / 4) + (i % 4));
-                if (a.out_scores) {
-                    float* dst = a.out_scores + (size_t)rid[CV(C)] * a.B;
+                        for (int i = 0; i < 16; ++i)
+                            top[CV(C)].push_ascending(acc[i], rowb + 8 * (i / 4) + (i % 4));
+                        if (a.out_scores) {
+                            float* dst = a.out_scores + (size_t)rid[CV(C)] * a.B;
 #pragma unroll
-                    for (int i = 0; i < 16; ++i)
-                        if (valid[CV(C)]) dst[rowb + 8 * (i / 4) + (i % 4)] = acc[i];
-                }
-            });
+                            for (int i = 0; i < 16; ++i)
+                                if (valid[CV(C)]) dst[rowb + 8 * (i / 4) + (i % 4)] = acc[i];
+                        }
+                    });
+            }
+        });
     }
     int sel[CB][NCAP];
     sfor<CB>([&](auto C) {
@@ -499,7 +597,7 @@ render_kernel(const RenderArgs a) {
             for (int c = 0; c < 3; ++c) x[c] = ray[cb].o[c] + tk[cb] * ray[cb].r[c];
             warp(a, x, w);
             float f[kSSlots];
-            fourier<5>(w, g, f);
+            fourier<5, !BF16>(w, g, f);
             f[30] = g ? w[2] : w[0];
             f[31] = g ? 0.0f : w[1];
 #pragma unroll
@@ -507,23 +605,23 @@ render_kernel(const RenderArgs a) {
         }
         {
             auto gs = [&](auto K, auto C) { return sin_[CV(K)][CV(C)]; };
-            hidden_layer<BF16, KS_S0>(st, lane, g, bias_s + s_bias, gs, h0);
+            hidden_layer<BF16, CB, KS_S0>(st, g, bias_s + s_bias, gs, h0);
         }
         for (int l = 0; l < 3; ++l) {
-            hidden_layer<BF16, KS_H>(st, lane, g, bias_s + s_bias + 256 * (1 + 2 * l), g0, h1);
-            hidden_layer<BF16, KS_H>(st, lane, g, bias_s + s_bias + 256 * (2 + 2 * l), g1, h0);
+            hidden_layer<BF16, CB, KS_H>(st, g, bias_s + s_bias + 256 * (1 + 2 * l), g0, h1);
+            hidden_layer<BF16, CB, KS_H>(st, g, bias_s + s_bias + 256 * (2 + 2 * l), g1, h0);
         }
         auto gh = [&](auto K, auto C) {
             if constexpr (CV(K) < KS_H) return h0[CV(K)][CV(C)];
             else return skip[CV(K) - KS_H][CV(C)];
         };
-        run_pass<BF16, KS_H + KS_SK, 1, 0>(
-            st, lane, g, bias_s + s_bias + 7 * 256, gh, [&](auto R, auto C, const f32x16& acc) {
+        run_pass<BF16, CB, KS_H + KS_SK, 1, 0>(
+            st, g, bias_s + s_bias + 7 * 256, gh, [&](auto R, auto C, const f32x16& acc) {
                 constexpr int cb = CV(C);
                 // lanes of group 0 hold rows 0..3 = (r, g, b, sigma) in registers 0..3
-                const float cr = 1.0f / (1.0f + __expf(-acc[0]));
-                const float cg = 1.0f / (1.0f + __expf(-acc[1]));
-                const float cbl = 1.0f / (1.0f + __expf(-acc[2]));
+                const float cr = 1.0f / (1.0f + expf(-acc[0]));
+                const float cg = 1.0f / (1.0f + expf(-acc[1]));
+                const float cbl = 1.0f / (1.0f + expf(-acc[2]));
                 const float sigma = fmaxf(acc[3], 0.0f);
                 const float tau = sigma * dk[cb];
                 const float alpha = -expm1f(-tau);
@@ -535,6 +633,7 @@ render_kernel(const RenderArgs a) {
                 T[cb] *= expf(-tau);
             });
     }
+    st.finish();  // no copy into LDS may outlive the workgroup
 
     // ---- outputs (lane group 0 holds the composited values)
 #pragma unroll
@@ -601,16 +700,16 @@ __global__ void __launch_bounds__(256) topn_kernel(const float* scores, int32_t 
 hipError_t launch_render(bool bf16, int ncap, const RenderArgs& a, hipStream_t stream) {
     const uint32_t rpb = (uint32_t)rays_per_block(bf16);
     const dim3 grid((a.total_rays + rpb - 1) / rpb);
-    const dim3 block(kThreads);
-#define DN_LAUNCH(B16, NC) hipLaunchKernelGGL((render_kernel<B16, NC>), grid, block, 0, stream, a)
+#define DN_LAUNCH(B16, CB, NW, OCC, NC) \
+    hipLaunchKernelGGL((render_kernel<B16, CB, NW, OCC, NC>), grid, dim3(64 * NW), 0, stream, a)
     if (bf16) {
-        if (ncap == 4) DN_LAUNCH(true, 4);
-        else if (ncap == 8) DN_LAUNCH(true, 8);
-        else DN_LAUNCH(true, 16);
+        if (ncap == 4) DN_LAUNCH(true, kBf16CB, kBf16NW, kBf16Occ, 4);
+        else if (ncap == 8) DN_LAUNCH(true, kBf16CB, kBf16NW, kBf16Occ, 8);
+        else DN_LAUNCH(true, kBf16CB, kBf16NW, kBf16Occ, 16);
     } else {
-        if (ncap == 4) DN_LAUNCH(false, 4);
-        else if (ncap == 8) DN_LAUNCH(false, 8);
-        else DN_LAUNCH(false, 16);
+        if (ncap == 4) DN_LAUNCH(false, 1, 4, 1, 4);
+        else if (ncap == 8) DN_LAUNCH(false, 1, 4, 1, 8);
+        else DN_LAUNCH(false, 1, 4, 1, 16);
     }
 #undef DN_LAUNCH
     return hipGetLastError();

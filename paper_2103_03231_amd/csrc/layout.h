@@ -33,9 +33,15 @@ constexpr int kSIn = 63;      // encode(warped sample, 10)
 constexpr int kSkip = 27;     // encode(dir, 4) into the last shading layer
 constexpr int kSOut = 4;      // r, g, b, sigma
 constexpr int kFragBytes = 1024;
-constexpr int kChunkFrags = 32;                 // fragments per streamed chunk
+#ifndef DONERF_CHUNK_FRAGS
+#define DONERF_CHUNK_FRAGS 32
+#endif
+#ifndef DONERF_RING
+#define DONERF_RING 3
+#endif
+constexpr int kChunkFrags = DONERF_CHUNK_FRAGS;  // fragments per streamed chunk
 constexpr int kChunkBytes = kChunkFrags * kFragBytes;
-constexpr int kRing = 3;                        // LDS chunk slots
+constexpr int kRing = DONERF_RING;               // LDS chunk slots (prefetch distance kRing - 1)
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kMaxPosesPerLaunch = 32;
