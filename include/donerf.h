@@ -3,10 +3,10 @@
  *
  * The library renders camera images with DONeRF (Neff et al., "DONeRF: Towards
  * Real-Time Rendering of Compact Neural Radiance Fields using Depth Oracle
- * Networks", EGSR 2021).  For every pixel ray (Sec. 3, Eq. 1) it
- *   1. moves the ray origin onto the sphere around the view cell (Sec. 4.2),
+ * Networks", EGSR 2021).  For every pixel ray (Sec. 4, Eq. 1) it
+ *   1. moves the ray origin onto the sphere around the view cell (Sec. 5.2),
  *   2. evaluates the depth-oracle network once on the encoded unified origin
- *      and direction, giving one score per logarithmic depth class (Sec. 4.1,
+ *      and direction, giving one score per logarithmic depth class (Sec. 5.1,
  *      Eq. 3 discretisation),
  *   3. keeps the N best-scoring classes and places one sample at the centre
  *      of each (Eq. 1 with the class centre as depth),
@@ -76,7 +76,7 @@ typedef struct donerf_cfg {
     float fov_x_deg;   /* horizontal field of view of the pinhole camera, in
                           degrees, 0 < fov < 180                               */
     float centre[3];   /* view-cell centre c (Eq. 2, Eq. 4)                    */
-    float radius;      /* radius > 0 of the unification sphere (Sec. 4.2)      */
+    float radius;      /* radius > 0 of the unification sphere (Sec. 5.2)      */
     int32_t precision; /* donerf_precision                                     */
     int32_t select;    /* donerf_select                                        */
 } donerf_cfg;

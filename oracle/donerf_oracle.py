@@ -6,16 +6,16 @@ The oracle shares no code with the HIP path.
 
 It follows DONeRF (Neff et al., EGSR 2021, arXiv 2103.03231) one step at a time:
 
-  ray through a pixel (Sec. 3, Eq. 1)
-  -> ray unification onto the view-cell sphere (Sec. 4.2, Fig. 8)
-  -> encoded depth-network input, normalised by d_max (Sec. 3, Eq. 2)
-  -> depth-oracle network, 8 linear layers of 256 units (Sec. 4.3, App. D)
-  -> log-discretised depth bins (Sec. 3, Eq. 3; Sec. 4.2) and top-N selection
+  ray through a pixel (Sec. 4, Eq. 1)
+  -> ray unification onto the view-cell sphere (Sec. 5.2, Fig. 8)
+  -> encoded depth-network input, normalised by d_max (Sec. 4, Eq. 2)
+  -> depth-oracle network, 8 linear layers of 256 units (Sec. 5.3, App. D)
+  -> log-discretised depth bins (Sec. 4, Eq. 3; Sec. 5.2) and top-N selection
   -> samples x = o + t r (Eq. 1) at the selected bin centres
-  -> space warp (Sec. 3, Eq. 4-5) and encoding
+  -> space warp (Sec. 4, Eq. 4-5) and encoding
   -> shading network with the encoded direction skipped into its last layer
      (App. D, Fig. 12)
-  -> alpha compositing with a black background (Sec. 2, Sec. 5.1).
+  -> alpha compositing with a black background (Sec. 3, Sec. 6.1).
 
 Precision.  Ray geometry (ray, unification, sample placement, warp) runs in
 fp32 with the operation order written below, so that a fp32 implementation
@@ -70,7 +70,7 @@ def log_depth(d, near, far):
 
 
 def bin_table(near, far, n_bins):
-    """Depth classes uniform in the log coordinate of Eq. 3 (Sec. 4.2 applies
+    """Depth classes uniform in the log coordinate of Eq. 3 (Sec. 5.2 applies
     the same transform to the classification steps).
 
     Boundaries are the inverse of Eq. 3 at B+1 uniform coordinates,
@@ -126,7 +126,7 @@ def dot3(a, b):
 
 
 def unify(o, r, centre, radius):
-    """Sec. 4.2, Fig. 8: move each ray origin onto the sphere of the given
+    """Sec. 5.2, Fig. 8: move each ray origin onto the sphere of the given
     radius around the view-cell centre, along the ray (the forward root of
     |o + t r - c| = R, clamped at t >= 0; the paper's case of rays looking out
     of the view cell)."""
@@ -250,7 +250,7 @@ def softmax_fp32(logits):
 # ---------------------------------------------------------------- compositing
 
 def composite(raw, t, delta):
-    """NeRF-style accumulation with a black background (Sec. 2, Sec. 5.1).
+    """NeRF-style accumulation with a black background (Sec. 3, Sec. 6.1).
 
     raw: (rays, N, 4) network outputs (r, g, b, sigma) in depth order;
     t, delta: (rays, N) sample depth and the width of its depth class.
@@ -284,7 +284,7 @@ def render_rays(d_layers, s_layers, o, r, N, near, far, n_bins, centre, radius,
     select='topn_softmax', probs (n,B) fp32."""
     d_max = F32(far)
     c = np.asarray(centre, dtype=F32)
-    # 1-2: unification and the encoded depth-network input (Eq. 2 / Sec. 4.2).
+    # 1-2: unification and the encoded depth-network input (Eq. 2 / Sec. 5.2).
     ou = unify(o, r, c, radius)
     v = ((ou - c) / d_max).astype(F32)
     enc_r = encode(r, L_DIR)

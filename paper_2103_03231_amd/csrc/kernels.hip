@@ -1,7 +1,7 @@
 // kernels.hip - DONeRF per-ray inference for gfx950 (MI355X).
 //
 // One fused kernel renders a tile of rays per workgroup: ray generation and
-// unification (Sec. 4.2), encoding of the depth-network input (Eq. 2), the
+// unification (Sec. 5.2), encoding of the depth-network input (Eq. 2), the
 // depth-oracle network (App. D) on MFMA, top-N selection of depth classes in
 // registers, sample placement at the class centres (Eq. 1, Eq. 3), the space
 // warp (Eq. 4-5) and encoding, the shading network on MFMA with the encoded
@@ -94,7 +94,10 @@ __device__ __forceinline__ void lds_barrier() {
 }
 
 constexpr int kChunkVec = kChunkBytes / 16;  // u32x4 per chunk
-constexpr int kFragAhead = 2;                 // LDS fragment reads in flight
+#ifndef DONERF_FRAG_AHEAD
+#define DONERF_FRAG_AHEAD 3
+#endif
+constexpr int kFragAhead = DONERF_FRAG_AHEAD;  // LDS fragment reads in flight
 
 // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
 template <int VM>
@@ -389,7 +392,7 @@ __device__ __forceinline__ Ray camera_ray(const RenderArgs& a, uint32_t ray) {
     return out;
 }
 
-// Sec. 4.2: the forward intersection with the sphere |x - c| = R, t >= 0.
+// Sec. 5.2: the forward intersection with the sphere |x - c| = R, t >= 0.
 __device__ __forceinline__ void unify(const RenderArgs& a, const Ray& ray, float (&ou)[3]) {
     const float q0 = ray.o[0] - a.cx, q1 = ray.o[1] - a.cy, q2 = ray.o[2] - a.cz;
     const float b = (ray.r[0] * q0 + ray.r[1] * q1) + ray.r[2] * q2;

@@ -12,7 +12,7 @@ It produces
 
 The paper's scenes and trained weights are not available; these generators
 stand in for them with the paper's resolutions (400x400 renders, Fig. 1 and
-Sec. 5; a 1440x1600-per-eye headset, Sec. 1) and random-init networks of the
+Sec. 6; a 1440x1600-per-eye headset, Sec. 1) and random-init networks of the
 paper's architecture (8 layers of 256 units, App. D).  Timing does not depend
 on weight values.
 """

@@ -103,7 +103,7 @@ def test_camera_horizontal_field_of_view():
     assert np.all(np.diff(col) < 0)
 
 
-# ------------------------------------------------------------------ unification (Sec. 4.2)
+# ------------------------------------------------------------------ unification (Sec. 5.2)
 
 def test_unify_lands_on_sphere_and_is_origin_invariant():
     rng = np.random.default_rng(1)
