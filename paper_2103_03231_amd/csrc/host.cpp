@@ -23,6 +23,8 @@ struct donerf_handle {
     float* bias;         // device
     float* bins;         // device: centres[B], widths[B]
     int n_d_chunks, n_s_chunks, bias_len;
+    int n_cu;            // compute units: workgroups of one full round
+    float* partial;      // device: split-tail parts, n_cu * 256 rays * 5 floats
     std::vector<float> h_bounds, h_centres, h_widths;
 };
 
@@ -214,8 +216,26 @@ int render_impl(donerf_t* h, const float* poses, int32_t P, int32_t H, int32_t W
         a.out_depth = out_depth ? out_depth + (size_t)p0 * hw : nullptr;
         a.out_bins = out_bins ? out_bins + (size_t)p0 * hw * N : nullptr;
         a.out_scores = out_scores ? out_scores + (size_t)p0 * hw * c.n_bins : nullptr;
-        hipError_t e = launch_render(h->bf16, ncap_for(N), a, h->stream);
+        // Full rounds of one workgroup per CU run as they are.  The tiles of a
+        // last, partial round are split by samples over up to n_cu / r
+        // workgroups each (every part recomputes the depth network), and a
+        // combine pass composites the parts.
+        const uint32_t rpb = (uint32_t)rays_per_block(h->bf16);
+        const uint32_t tiles = (a.total_rays + rpb - 1) / rpb;
+        const uint32_t round = (uint32_t)h->n_cu;
+        const uint32_t full = tiles / round * round, rem = tiles - full;
+        uint32_t split = rem ? round / rem : 1;
+        if (split > (uint32_t)N) split = (uint32_t)N;
+        if (split < 1) split = 1;
+        a.n_full = split > 1 ? full : tiles;
+        a.split = (int32_t)split;
+        a.partial = h->partial;
+        hipError_t e = launch_render(h->bf16, ncap_for(N), a, split > 1 ? rem : 0, h->stream);
         if (e != hipSuccess) return hip_fail(e, "render launch");
+        if (split > 1) {
+            e = launch_combine(h->bf16, a, h->stream);
+            if (e != hipSuccess) return hip_fail(e, "combine launch");
+        }
         if (out_scores && c.select == DONERF_SELECT_TOPN_SOFTMAX) {
             e = launch_softmax_rows(a.out_scores, a.total_rays, c.n_bins, h->stream);
             if (e != hipSuccess) return hip_fail(e, "softmax launch");
@@ -287,7 +307,13 @@ int donerf_create(const donerf_cfg* cfg, const float* weights, size_t n_weights,
     std::memcpy(bins.data() + B, h->h_widths.data(), sizeof(float) * B);
 
     hipError_t e;
+    if ((e = hipDeviceGetAttribute(&h->n_cu, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess ||
+        h->n_cu < 1) {
+        donerf_destroy(h);
+        return hip_fail(e, "hipDeviceGetAttribute");
+    }
     if ((e = hipMalloc(&h->d_frags, frags.size())) != hipSuccess ||
+        (e = hipMalloc(&h->partial, sizeof(float) * 5 * 256 * (size_t)h->n_cu)) != hipSuccess ||
         (e = hipMalloc(&h->bias, sizeof(float) * bias.size())) != hipSuccess ||
         (e = hipMalloc(&h->bins, sizeof(float) * bins.size())) != hipSuccess) {
         donerf_destroy(h);
@@ -308,6 +334,7 @@ void donerf_destroy(donerf_t* h) {
     if (h->d_frags) (void)hipFree(h->d_frags);
     if (h->bias) (void)hipFree(h->bias);
     if (h->bins) (void)hipFree(h->bins);
+    if (h->partial) (void)hipFree(h->partial);
     delete h;
 }
 

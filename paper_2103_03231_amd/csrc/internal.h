@@ -24,6 +24,15 @@ struct RenderArgs {
     int32_t bias_len;       // floats in bias
     int32_t H, W, n_poses, N, B;
     uint32_t total_rays;    // n_poses * H * W
+    // Workgroups b < n_full render tile b whole.  Workgroups b >= n_full
+    // split the remaining tiles by samples: with c = b - n_full, tile
+    // n_full + c / split, samples [j N / split, (j + 1) N / split) for
+    // j = c % split.  With split > 1 such a part writes its composite (C rgb,
+    // depth, transmittance) to partial[(local_ray * split + j) * 5], local_ray
+    // counted from the first ray of tile n_full, instead of the outputs.
+    uint32_t n_full;
+    int32_t split;
+    float* partial;
     float focal, half_w, half_h;
     float cx, cy, cz;
     float radius;
@@ -49,7 +58,11 @@ constexpr int kBf16Occ = DONERF_BF16_OCC;
 // Rays handled by one workgroup.
 inline int rays_per_block(bool bf16) { return bf16 ? kBf16NW * 32 * kBf16CB : 4 * 32; }
 
-hipError_t launch_render(bool bf16, int ncap, const RenderArgs& a, hipStream_t stream);
+// Launches a.n_full whole tiles plus n_split_tiles tiles split a.split ways.
+hipError_t launch_render(bool bf16, int ncap, const RenderArgs& a, uint32_t n_split_tiles, hipStream_t stream);
+// Composites the split parts of rays [n_full * rays_per_block, total_rays)
+// into out_rgb / out_depth.
+hipError_t launch_combine(bool bf16, const RenderArgs& a, hipStream_t stream);
 hipError_t launch_softmax_rows(float* scores, uint32_t rows, int B, hipStream_t stream);
 hipError_t launch_topn(bool bf16_layout, int ncap, const float* scores, int32_t rays,
                        int32_t N, int32_t B, int32_t* out_idx, hipStream_t stream);

@@ -487,13 +487,22 @@ render_kernel(const RenderArgs a) {
     st.ring = ring;
     st.nd = a.n_d_chunks;
     st.ns = a.n_s_chunks;
-    st.total = a.n_d_chunks + a.N * a.n_s_chunks;
+    // this workgroup's tile and its share of the samples
+    const bool split_part = blockIdx.x >= a.n_full;
+    const uint32_t cpart = blockIdx.x - a.n_full;
+    const int nsplit = split_part ? a.split : 1;
+    const int part = split_part ? (int)(cpart % (uint32_t)a.split) : 0;
+    const uint32_t tile_local = split_part ? cpart / (uint32_t)a.split : 0;
+    const uint32_t tile = split_part ? a.n_full + tile_local : blockIdx.x;
+    const int k_begin = part * a.N / nsplit;
+    const int k_end = (part + 1) * a.N / nsplit;
+    st.total = a.n_d_chunks + (k_end - k_begin) * a.n_s_chunks;
     st.lane = lane;
     st.wave = wave;
     st.start();
 
     // ---- rays of this wave: column col of block cb
-    const uint32_t ray0 = ((uint32_t)blockIdx.x * NW + wave) * (32 * CB);
+    const uint32_t ray0 = (tile * NW + wave) * (32 * CB);
     uint32_t rid[CB];
     bool valid[CB];
     Ray ray[CB];
@@ -563,7 +572,7 @@ render_kernel(const RenderArgs a) {
 #pragma unroll
                         for (int i = 0; i < 16; ++i)
                             top[CV(C)].push_ascending(acc[i], rowb + 8 * (i / 4) + (i % 4));
-                        if (a.out_scores) {
+                        if (a.out_scores && part == 0) {
                             float* dst = a.out_scores + (size_t)rid[CV(C)] * a.B;
 #pragma unroll
                             for (int i = 0; i < 16; ++i)
@@ -585,7 +594,7 @@ render_kernel(const RenderArgs a) {
 #pragma unroll
     for (int cb = 0; cb < CB; ++cb) T[cb] = 1.0f, Cr[cb] = Cg[cb] = Cb[cb] = Dp[cb] = 0.0f;
 
-    for (int k = 0; k < a.N; ++k) {
+    for (int k = k_begin; k < k_end; ++k) {
         u32x4 sin_[KS_S0][CB];
         float tk[CB], dk[CB];
 #pragma unroll
@@ -642,16 +651,48 @@ render_kernel(const RenderArgs a) {
 #pragma unroll
     for (int cb = 0; cb < CB; ++cb) {
         if (g == 0 && valid[cb]) {
-            float* o = a.out_rgb + (size_t)rid[cb] * 3;
-            o[0] = Cr[cb];
-            o[1] = Cg[cb];
-            o[2] = Cb[cb];
-            if (a.out_depth) a.out_depth[rid[cb]] = Dp[cb];
-            if (a.out_bins) {
+            if (nsplit > 1) {
+                const uint32_t local = tile_local * (32 * CB * NW) + wave * (32 * CB) + 32 * cb + col;
+                float* q = a.partial + ((size_t)local * nsplit + part) * 5;
+                q[0] = Cr[cb];
+                q[1] = Cg[cb];
+                q[2] = Cb[cb];
+                q[3] = Dp[cb];
+                q[4] = T[cb];
+            } else {
+                float* o = a.out_rgb + (size_t)rid[cb] * 3;
+                o[0] = Cr[cb];
+                o[1] = Cg[cb];
+                o[2] = Cb[cb];
+                if (a.out_depth) a.out_depth[rid[cb]] = Dp[cb];
+            }
+            if (a.out_bins && part == 0) {
                 for (int k = 0; k < a.N; ++k) a.out_bins[(size_t)rid[cb] * a.N + k] = pick(sel[cb], k);
             }
         }
     }
+}
+
+// Front-to-back composite of the split parts of a ray: C = C_0 + T_0 (C_1 +
+// T_1 (C_2 + ...)), the same recurrence the render kernel runs per sample.
+__global__ void combine_kernel(const float* partial, int split, uint32_t first_ray, uint32_t total_rays,
+                               float* out_rgb, float* out_depth) {
+    const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    const uint32_t ray = first_ray + i;
+    if (ray >= total_rays) return;
+    float T = 1.0f, c0 = 0.0f, c1 = 0.0f, c2 = 0.0f, d = 0.0f;
+    for (int j = 0; j < split; ++j) {
+        const float* q = partial + ((size_t)i * split + j) * 5;
+        c0 += T * q[0];
+        c1 += T * q[1];
+        c2 += T * q[2];
+        d += T * q[3];
+        T *= q[4];
+    }
+    out_rgb[(size_t)ray * 3 + 0] = c0;
+    out_rgb[(size_t)ray * 3 + 1] = c1;
+    out_rgb[(size_t)ray * 3 + 2] = c2;
+    if (out_depth) out_depth[ray] = d;
 }
 
 // Softmax of each score row in place (fp32: subtract the row maximum,
@@ -700,9 +741,8 @@ __global__ void __launch_bounds__(256) topn_kernel(const float* scores, int32_t 
 
 }  // namespace
 
-hipError_t launch_render(bool bf16, int ncap, const RenderArgs& a, hipStream_t stream) {
-    const uint32_t rpb = (uint32_t)rays_per_block(bf16);
-    const dim3 grid((a.total_rays + rpb - 1) / rpb);
+hipError_t launch_render(bool bf16, int ncap, const RenderArgs& a, uint32_t n_split_tiles, hipStream_t stream) {
+    const dim3 grid(a.n_full + n_split_tiles * (uint32_t)a.split);
 #define DN_LAUNCH(B16, CB, NW, OCC, NC) \
     hipLaunchKernelGGL((render_kernel<B16, CB, NW, OCC, NC>), grid, dim3(64 * NW), 0, stream, a)
     if (bf16) {
@@ -715,6 +755,14 @@ hipError_t launch_render(bool bf16, int ncap, const RenderArgs& a, hipStream_t s
         else DN_LAUNCH(false, 1, 4, 1, 16);
     }
 #undef DN_LAUNCH
+    return hipGetLastError();
+}
+
+hipError_t launch_combine(bool bf16, const RenderArgs& a, hipStream_t stream) {
+    const uint32_t first = a.n_full * (uint32_t)rays_per_block(bf16);
+    const uint32_t n = a.total_rays - first;
+    hipLaunchKernelGGL(combine_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, a.partial, a.split, first,
+                       a.total_rays, a.out_rgb, a.out_depth);
     return hipGetLastError();
 }
 
