@@ -26,6 +26,25 @@ sys.path.insert(0, ROOT)
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}   # MI355X dense peaks
 HBM_PEAK_GBS = 8000.0
 
+# HBM bytes per render dispatch of the default workload, from two
+# rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE; profiles/
+# render_kernel_frame400_n4_bf16_traffic.md) scaled by the same counters on a
+# plain 256 MiB copy (FETCH_SIZE reads half the bytes moved: x2; WRITE_SIZE
+# exact: x1).  Valid only for the kernel sources they were taken on.
+MEASURED_TRAFFIC = {"sources_sha256_16": "9ff151d5d842dbc3", "workload": "frame400_n4_bf16",
+                    "fetch_kib": 7330.8 * 2, "write_kib": 11760.0}
+KERNEL_SOURCES = ("paper_2103_03231_amd/csrc/kernels.hip", "paper_2103_03231_amd/csrc/layout.h",
+                  "paper_2103_03231_amd/csrc/internal.h")
+
+
+def kernel_sources_sha() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
 
 def algorithmic_flop_per_ray(N: int, n_bins: int) -> int:
     """2 x multiply-adds of both networks for one ray (8 layers of 256 units):
@@ -75,7 +94,23 @@ def main():
     ap.add_argument("--workload", default="frame400_n4_bf16")
     ap.add_argument("--cpu-sample", type=int, default=262144)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB (3 times), to calibrate the "
+                         "FETCH_SIZE / WRITE_SIZE counters against known bytes")
+    ap.add_argument("--traffic-kib", type=float, nargs=2, default=None, metavar=("FETCH", "WRITE"),
+                    help="HBM KiB per render dispatch from the calibrated FETCH_SIZE and WRITE_SIZE "
+                         "counters of the current kernel, reported as roofline.traffic")
     args = ap.parse_args()
+    if args.copy_calibration:
+        import torch
+        n = args.copy_calibration * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes_read": n * 4, "bytes_written": n * 4, "repeats": 3}))
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only: the rays of a frame are "
                                    "independent, so several GPUs would each render a share of the "
@@ -126,6 +161,13 @@ def main():
     achieved = flop_launch / (avg_kern_ms * 1e-3) / 1e12
     peak = MFMA_PEAK_TFLOPS[wl.precision]
     paper_mrays = 400 * 400 / 22e-3 / 1e6   # 22 ms per 400x400 frame, N = 4
+    traffic = None
+    kib = args.traffic_kib
+    if kib is None and (MEASURED_TRAFFIC["workload"] == wl.name
+                        and MEASURED_TRAFFIC["sources_sha256_16"] == kernel_sources_sha()):
+        kib = (MEASURED_TRAFFIC["fetch_kib"], MEASURED_TRAFFIC["write_kib"])
+    if kib is not None:
+        traffic = round((kib[0] + kib[1]) * 1024)
     line = {
         "metric": "Mrays/s + ms/frame at 400x400 N=4 (8x256 MLPs); MFMA util % of peak",
         "value": round(value, 3),
@@ -146,7 +188,8 @@ def main():
                    "algorithmic_mflop_per_ray": round(algorithmic_flop_per_ray(wl.N, wl.n_bins) / 1e6, 4),
                    "padded_mflop_per_ray": round(padded_flop_per_ray(wl.N, wl.n_bins) / 1e6, 4)},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
-                     "frac": round(achieved / peak, 4), "traffic": None,
+                     "frac": round(achieved / peak, 4),
+                     "traffic": traffic,
                      "kernel": "render_kernel<bf16>", "kernel_ms": round(avg_kern_ms, 4)},
     }
     if not args.no_cpu:
