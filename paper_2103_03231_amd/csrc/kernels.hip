@@ -221,39 +221,11 @@ __device__ __forceinline__ void run_pass(WS& st, int g, const float* bias, GetB&
     sfor<RBP>([&](auto R) { sfor<CB>([&](auto C) { epi(R, C, acc[CV(R)][CV(C)]); }); });
 }
 
-// Activation storage in accumulation registers.  With 64 rays per wave the
-// two activation arrays of a layer (input and output, 128 registers each)
-// do not both fit in the 256 architectural VGPRs, so the output array is
-// built in AGPRs and copied back once per layer.  The MFMAs stay compiler
-// builtins (the compiler keeps their hazard handling); only these moves are
-// written out.  The copy back ends with s_nop 1, covering the wait states
-// between a VALU write of a VGPR and an MFMA reading it.
-#ifndef DONERF_ACT_AGPR
-#define DONERF_ACT_AGPR 1
-#endif
-__device__ __forceinline__ uint32_t to_agpr(uint32_t v) {
-    uint32_t r;
-    asm("v_accvgpr_write_b32 %0, %1" : "=a"(r) : "v"(v));
-    return r;
-}
-__device__ __forceinline__ u32x4 from_agpr(u32x4 a) {
-    u32x4 r;
-    asm volatile(
-        "v_accvgpr_read_b32 %0, %4\n\t"
-        "v_accvgpr_read_b32 %1, %5\n\t"
-        "v_accvgpr_read_b32 %2, %6\n\t"
-        "v_accvgpr_read_b32 %3, %7\n\t"
-        "s_nop 1"
-        : "=v"(r[0]), "=v"(r[1]), "=v"(r[2]), "=v"(r[3])
-        : "a"(a[0]), "a"(a[1]), "a"(a[2]), "a"(a[3]));
-    return r;
-}
-
 // ReLU, round, and place a 32-row accumulator block as K steps
 // [ks0, ks0 + KSPB) of the next layer's B operand.  bf16: round to nearest
 // even, then ReLU on the packed pair as a signed 16-bit max with 0 (rounding
 // preserves the sign, so this equals rounding the ReLU).
-template <bool BF16, bool AG, int NK, int CB>
+template <bool BF16, int NK, int CB>
 __device__ __forceinline__ void emit_relu(const f32x16& acc, u32x4 (&out)[NK][CB], int ks0, int cb) {
     using P = Prec<BF16>;
     if constexpr (BF16) {
@@ -264,8 +236,7 @@ __device__ __forceinline__ void emit_relu(const f32x16& acc, u32x4 (&out)[NK][CB
 #pragma unroll
             for (int w = 0; w < 4; ++w) {
                 const i16x2 v = __builtin_bit_cast(i16x2, pack_bf16x2(acc[8 * h + 2 * w], acc[8 * h + 2 * w + 1]));
-                const uint32_t x = __builtin_bit_cast(uint32_t, __builtin_elementwise_max(v, i16x2{0, 0}));
-                o[w] = AG ? to_agpr(x) : x;
+                o[w] = __builtin_bit_cast(uint32_t, __builtin_elementwise_max(v, i16x2{0, 0}));
             }
             out[ks0 + h][cb] = o;
         }
@@ -283,7 +254,7 @@ __device__ __forceinline__ void emit_relu(const f32x16& acc, u32x4 (&out)[NK][CB
 // alternating accumulator sets, so the bias/ReLU/rounding of pass p can
 // overlap the MFMAs of pass p + 1, and LDS reads run kFragAhead fragments
 // ahead across pass and chunk boundaries.
-template <bool BF16, int CB, int KS, bool AG = false, class WS, class GetB>
+template <bool BF16, int CB, int KS, class WS, class GetB>
 __device__ __forceinline__ void hidden_layer(WS& st, int g, const float* bias, GetB&& getB,
                                              u32x4 (&out)[8 * Prec<BF16>::KSPB][CB]) {
     using P = Prec<BF16>;
@@ -315,7 +286,7 @@ __device__ __forceinline__ void hidden_layer(WS& st, int g, const float* bias, G
             if constexpr (w == PF - 1) {
                 sfor<RBP>([&](auto R) {
                     sfor<CB>([&](auto C) {
-                        emit_relu<BF16, AG>(acc[p & 1][CV(R)][CV(C)], out, (p * RBP + CV(R)) * P::KSPB, CV(C));
+                        emit_relu<BF16>(acc[p & 1][CV(R)][CV(C)], out, (p * RBP + CV(R)) * P::KSPB, CV(C));
                     });
                 });
             }
@@ -581,37 +552,20 @@ render_kernel(const RenderArgs a) {
     lds_barrier();  // bias_s and bins_s visible
 
     // ---- depth-oracle network
-    // h0 holds the input of the next layer.  AG: layers write h1 (AGPRs),
-    // copied into h0 afterwards; otherwise layers alternate h0 -> h1 -> h0.
-    constexpr bool AG = BF16 && CB == 2 && DONERF_ACT_AGPR;
+    // Layers alternate h0 -> h1 -> h0; h0 holds the input of the next layer.
     u32x4 h0[KS_H][CB], h1[KS_H][CB];
     auto g0 = [&](auto K, auto C) { return h0[CV(K)][CV(C)]; };
     auto g1 = [&](auto K, auto C) { return h1[CV(K)][CV(C)]; };
-    auto h1_to_h0 = [&]() {
-        sfor<KS_H>([&](auto K) { sfor<CB>([&](auto C) { h0[CV(K)][CV(C)] = from_agpr(h1[CV(K)][CV(C)]); }); });
-    };
     // six 256 -> 256 ReLU layers whose biases start at bias_l0
     auto hidden6 = [&](const float* bias_l0) {
-        if constexpr (AG) {
-            for (int l = 0; l < 6; ++l) {
-                hidden_layer<BF16, CB, KS_H, true>(st, g, bias_l0 + 256 * l, g0, h1);
-                h1_to_h0();
-            }
-        } else {
-            for (int l = 0; l < 3; ++l) {
-                hidden_layer<BF16, CB, KS_H>(st, g, bias_l0 + 256 * (2 * l), g0, h1);
-                hidden_layer<BF16, CB, KS_H>(st, g, bias_l0 + 256 * (2 * l + 1), g1, h0);
-            }
+        for (int l = 0; l < 3; ++l) {
+            hidden_layer<BF16, CB, KS_H>(st, g, bias_l0 + 256 * (2 * l), g0, h1);
+            hidden_layer<BF16, CB, KS_H>(st, g, bias_l0 + 256 * (2 * l + 1), g1, h0);
         }
     };
     {
         auto gin = [&](auto K, auto C) { return din[CV(K)][CV(C)]; };
-        if constexpr (AG) {
-            hidden_layer<BF16, CB, KS_D0, true>(st, g, bias_s, gin, h1);
-            h1_to_h0();
-        } else {
-            hidden_layer<BF16, CB, KS_D0>(st, g, bias_s, gin, h0);
-        }
+        hidden_layer<BF16, CB, KS_D0>(st, g, bias_s, gin, h0);
     }
     hidden6(bias_s + 256);
     TopList<NCAP> top[CB];
@@ -627,8 +581,8 @@ render_kernel(const RenderArgs a) {
             const int p = p0 + q;
             if (p < npass) {
                 run_pass<BF16, CB, KS_H, kRbPerPass, q * PASS_FRAGS>(
-                    st, g, bias_s + 7 * 256 + 64 * p, g0, [&](auto R, auto C, const f32x16& acc) {
-                        const int rowb = 64 * p + 32 * CV(R) + 4 * g;
+                    st, g, bias_s + 7 * 256 + 32 * kRbPerPass * p, g0, [&](auto R, auto C, const f32x16& acc) {
+                        const int rowb = 32 * kRbPerPass * p + 32 * CV(R) + 4 * g;
 #pragma unroll
                         for (int i = 0; i < 16; ++i)
                             top[CV(C)].push_ascending(acc[i], rowb + 8 * (i / 4) + (i % 4));
@@ -677,12 +631,7 @@ render_kernel(const RenderArgs a) {
         }
         {
             auto gs = [&](auto K, auto C) { return sin_[CV(K)][CV(C)]; };
-            if constexpr (AG) {
-                hidden_layer<BF16, CB, KS_S0, true>(st, g, bias_s + s_bias, gs, h1);
-                h1_to_h0();
-            } else {
-                hidden_layer<BF16, CB, KS_S0>(st, g, bias_s + s_bias, gs, h0);
-            }
+            hidden_layer<BF16, CB, KS_S0>(st, g, bias_s + s_bias, gs, h0);
         }
         hidden6(bias_s + s_bias + 256);
         auto gh = [&](auto K, auto C) {

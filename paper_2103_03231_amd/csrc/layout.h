@@ -45,7 +45,10 @@ constexpr int kRing = DONERF_RING;               // LDS chunk slots (prefetch di
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kMaxPosesPerLaunch = 32;
-constexpr int kRbPerPass = 2;                   // 32-row blocks per accumulator pass
+#ifndef DONERF_RB_PER_PASS
+#define DONERF_RB_PER_PASS 2
+#endif
+constexpr int kRbPerPass = DONERF_RB_PER_PASS;  // 32-row blocks per accumulator pass
 
 // Elements per lane per fragment and K per fragment.
 DN_HD constexpr int elems(bool bf16) { return bf16 ? 8 : 4; }

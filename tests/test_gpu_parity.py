@@ -242,3 +242,21 @@ def test_hd1080_n4_softmax_bf16_sampled():
 
 def test_stereo_n16_b256_bf16_sampled():
     _sampled("stereo1440x1600_n16_b256_bf16", 800)
+
+
+def test_split_tail_matches_whole_tiles():
+    """The same rays rendered whole (in full rounds of one workgroup per CU)
+    and split by samples (a launch's partial last round) agree to fp32
+    rounding of the compositing."""
+    r, _ = renderer("bf16", n_max=8)
+    pose = inputs.make_poses([6])
+    H, W, N = 64, 64, 8
+    alone = gpu_render(r, pose, H, W, N)                          # 16 tiles: split 8 ways
+    batch = gpu_render(r, np.repeat(pose, 32, axis=0), H, W, N)  # 512 tiles: two whole rounds
+    for idx in (0, 31):
+        other = {k: v.reshape(32, -1)[idx] for k, v in batch.items()}
+        for k in ("bins", "scores"):
+            assert np.array_equal(alone[k].reshape(-1), other[k]), k
+        np.testing.assert_allclose(alone["rgb"].reshape(-1), other["rgb"], rtol=0, atol=2e-6)
+        np.testing.assert_allclose(alone["depth"].reshape(-1), other["depth"], rtol=0, atol=2e-5)
+    r.close()
