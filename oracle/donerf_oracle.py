@@ -247,6 +247,56 @@ def softmax_fp32(logits):
     return (e / s).astype(F32)
 
 
+# ---------------------------------------------------------------- inverse-CDF placement
+
+def cdf_samples(logits, N, near, far):
+    """Sample placement of Sec. 5.1 (Fig. 7): the depth network's class values,
+    sigmoid(score) (the network is trained with binary cross-entropy), taken
+    as a piecewise-constant PDF over the classes, which are uniform in the
+    coordinate of Eq. 3; the CDF is inverted at the uniform steps
+    u_i = (i + 0.5) / N.  Each sample stands for the probability slice
+    [i/N, (i+1)/N]; its width is the depth extent of that slice.
+
+    Returns t (rays, N), delta (rays, N) and the class of each sample, fp64.
+    near/far are taken as fp32 values first."""
+    near = float(F32(near))
+    far = float(F32(far))
+    x = np.asarray(logits, dtype=np.float64)
+    p = 1.0 / (1.0 + np.exp(-x))
+    rays, B = p.shape
+    cdf = np.concatenate([np.zeros((rays, 1)), np.cumsum(p, axis=1)], axis=1)
+    cdf /= cdf[:, -1:]
+
+    def inverse(u):
+        # class k with cdf[k] <= u < cdf[k+1], so that cdf[k+1] > cdf[k]; the
+        # ends u = 0 and u = 1 map to the near and far ends by definition
+        # (numerically empty trailing classes would make the last step 0/0)
+        if u >= 1.0:
+            return np.ones(rays), np.full(rays, B - 1, dtype=np.int64)
+        k = np.empty(rays, dtype=np.int64)
+        for r in range(rays):
+            k[r] = np.searchsorted(cdf[r], u, side="right") - 1
+        k = np.clip(k, 0, B - 1)
+        lo = cdf[np.arange(rays), k]
+        hi = cdf[np.arange(rays), k + 1]
+        frac = np.clip((u - lo) / (hi - lo), 0.0, 1.0)
+        return (k + frac) / B, k
+
+    span = far - near
+    to_depth = lambda s: near + np.power(span + 1.0, s) - 1.0   # inverse of Eq. 3
+    t = np.empty((rays, N))
+    cls = np.empty((rays, N), dtype=np.int32)
+    edges = np.empty((rays, N + 1))
+    for i in range(N):
+        s_mid, k = inverse((i + 0.5) / N)
+        t[:, i] = to_depth(s_mid)
+        cls[:, i] = k
+    for i in range(N + 1):
+        s_edge, _ = inverse(i / N)
+        edges[:, i] = to_depth(s_edge)
+    return t, np.diff(edges, axis=1), cls
+
+
 # ---------------------------------------------------------------- compositing
 
 def composite(raw, t, delta):
@@ -278,10 +328,12 @@ def composite(raw, t, delta):
 # ---------------------------------------------------------------- full path
 
 def render_rays(d_layers, s_layers, o, r, N, near, far, n_bins, centre, radius,
-                precision="fp64", select="topn", forced_bins=None):
+                precision="fp64", select="topn", forced_bins=None, forced_samples=None):
     """Per-ray inference for rays (o, r) (fp32, (n, 3)).  Returns dict with
-    rgb (n,3), depth (n,), bins (n,N) int32, logits (n,B) fp64 and, for
-    select='topn_softmax', probs (n,B) fp32."""
+    rgb (n,3), depth (n,), bins (n,N) int32, logits (n,B) fp64, the sample
+    depths t and widths delta (n,N) and, for select='topn_softmax', probs
+    (n,B) fp32.  select='cdf' places samples by the inverse CDF (Sec. 5.1).
+    forced_samples = (t, delta) overrides the placement (for comparisons)."""
     d_max = F32(far)
     c = np.asarray(centre, dtype=F32)
     # 1-2: unification and the encoded depth-network input (Eq. 2 / Sec. 5.2).
@@ -296,14 +348,23 @@ def render_rays(d_layers, s_layers, o, r, N, near, far, n_bins, centre, radius,
     lg32 = logits.astype(F32)
     if select == "topn_softmax":
         out["probs"] = softmax_fp32(lg32)
-    elif select != "topn":
+    elif select not in ("topn", "cdf"):
         raise ValueError(select)
-    bins = topn(lg32, N) if forced_bins is None else np.asarray(forced_bins, dtype=np.int32)
+    if select == "cdf":
+        # 4-5: samples by the inverse CDF of the class values (Sec. 5.1).
+        t, delta, bins = cdf_samples(lg32, N, near, far)
+    else:
+        bins = topn(lg32, N) if forced_bins is None else np.asarray(forced_bins, dtype=np.int32)
+        # 5: samples at the selected class centres (Eq. 1, Eq. 3).
+        _, centres, widths = bin_table(near, far, n_bins)
+        t = centres[bins]
+        delta = widths[bins]
+    if forced_samples is not None:
+        t, delta = (np.asarray(a) for a in forced_samples)
     out["bins"] = bins
-    # 5: samples at the selected class centres (Eq. 1, Eq. 3).
-    _, centres, widths = bin_table(near, far, n_bins)
-    t = centres[bins]
-    delta = widths[bins]
+    out["t"] = np.asarray(t, dtype=np.float64)
+    out["delta"] = np.asarray(delta, dtype=np.float64)
+    t = np.asarray(t, dtype=F32)
     x = sample_points(o, r, t).astype(F32)
     # 6: space warp (Eq. 4-5) and encoding.
     w = warp(x, c, d_max)
@@ -320,7 +381,7 @@ def render_rays(d_layers, s_layers, o, r, N, near, far, n_bins, centre, radius,
 
 def render(weights, poses, H, W, N, n_bins=128, near=0.1, far=10.0, fov_x_deg=60.0,
            centre=(0.0, 0.0, 0.0), radius=1.5, precision="fp64", select="topn",
-           forced_bins=None, ray_subset=None, chunk=8192):
+           forced_bins=None, ray_subset=None, chunk=8192, forced_samples=None):
     """Render P poses (P, 3, 4) of H x W rays.  Returns rgb (P*H*W, 3), depth,
     bins and logits for every ray (or for ``ray_subset``, global ray ids)."""
     d_layers, s_layers = split_weights(weights, n_bins)
@@ -335,12 +396,14 @@ def render(weights, poses, H, W, N, n_bins=128, near=0.1, far=10.0, fov_x_deg=60
         o[sel] = po[ids[sel] - pi * hw]
         r[sel] = pr[ids[sel] - pi * hw]
     fb = None if forced_bins is None else np.asarray(forced_bins)
+    fs = None if forced_samples is None else tuple(np.asarray(a) for a in forced_samples)
     res = {}
     for s in range(0, len(ids), chunk):
         sl = slice(s, s + chunk)
         part = render_rays(d_layers, s_layers, o[sl], r[sl], N, near, far, n_bins,
                            centre, radius, precision, select,
-                           None if fb is None else fb[s:s + chunk])
+                           None if fb is None else fb[s:s + chunk],
+                           None if fs is None else (fs[0][sl], fs[1][sl]))
         for k, val in part.items():
             res.setdefault(k, []).append(val)
     return {k: np.concatenate(v) for k, v in res.items()}
