@@ -57,10 +57,19 @@ typedef enum donerf_precision {
 } donerf_precision;
 
 typedef enum donerf_select {
-    DONERF_SELECT_TOPN = 0,        /* N highest class scores                   */
-    DONERF_SELECT_TOPN_SOFTMAX = 1 /* the same classes, ranked on the softmax of
-                                      the scores (strictly monotone, so the
-                                      selection equals DONERF_SELECT_TOPN)     */
+    DONERF_SELECT_TOPN = 0,         /* one sample at the centre of each of the N
+                                       highest-scoring classes; its width is
+                                       the class width                          */
+    DONERF_SELECT_TOPN_SOFTMAX = 1, /* the same classes, ranked on the softmax
+                                       of the scores (strictly monotone, so the
+                                       selection equals DONERF_SELECT_TOPN)     */
+    DONERF_SELECT_CDF = 2           /* Sec. 5.1, Fig. 7: the class values
+                                       sigmoid(score) as a piecewise-constant
+                                       PDF over the classes (uniform in the
+                                       coordinate of Eq. 3), its CDF inverted at
+                                       u_i = (i + 0.5)/N; sample i's width is the
+                                       depth extent of the slice [i/N, (i+1)/N].
+                                       fp32 arithmetic; n_bins <= 128          */
 } donerf_select;
 
 /* Maximum number of samples per ray a handle can be created for. */
@@ -107,7 +116,7 @@ size_t donerf_weight_count(int32_t n_bins);
  *             on return
  *   out       receives the handle; set to NULL on failure
  * Errors: E_INVALID_ARG (NULL, cfg ranges), E_UNSUPPORTED (n_bins not in the
- * supported set), E_SIZE (n_weights != donerf_weight_count(cfg->n_bins)),
+ * supported set, or above 128 with DONERF_SELECT_CDF), E_SIZE (n_weights != donerf_weight_count(cfg->n_bins)),
  * E_NONFINITE (NaN/Inf in cfg or weights), E_DEVICE (no device or not
  * gfx950), E_NOMEM, E_HIP.
  */
@@ -143,15 +152,17 @@ int donerf_render(donerf_t* h, const float* cam_poses, int32_t P, int32_t H, int
 
 /*
  * donerf_render with optional per-ray intermediate outputs, for testing.
- *   out_bins    device, P x H x W x N int32: the selected depth classes in
- *               ascending order (= sample order), or NULL
- *   out_scores  device, P x H x W x B fp32: depth-network scores, or NULL;
- *               with DONERF_SELECT_TOPN_SOFTMAX the softmax probabilities
+ *   out_bins     device, P x H x W x N int32: the class of each sample in sample
+ *                (= depth) order, or NULL
+ *   out_scores   device, P x H x W x B fp32: depth-network scores, or NULL;
+ *                with DONERF_SELECT_TOPN_SOFTMAX the softmax probabilities
+ *   out_samples  device, P x H x W x N x 2 fp32: depth and width of each
+ *                sample, or NULL
  * Same errors as donerf_render.
  */
 int donerf_render_debug(donerf_t* h, const float* cam_poses, int32_t P, int32_t H,
                         int32_t W, int32_t N, float* out_rgb, float* out_depth,
-                        int32_t* out_bins, float* out_scores);
+                        int32_t* out_bins, float* out_scores, float* out_samples);
 
 /*
  * Run the device top-N selection on given scores, for testing.

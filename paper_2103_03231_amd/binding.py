@@ -29,6 +29,7 @@ FP32 = 0
 BF16 = 1
 SELECT_TOPN = 0
 SELECT_TOPN_SOFTMAX = 1
+SELECT_CDF = 2
 MAX_SAMPLES = 16
 
 # Every function include/donerf.h declares.
@@ -96,7 +97,7 @@ def lib():
         L.donerf_set_stream.argtypes, L.donerf_set_stream.restype = [vp, vp], ctypes.c_int
         L.donerf_render.argtypes = [vp, fp, i32, i32, i32, i32, vp, vp]
         L.donerf_render.restype = ctypes.c_int
-        L.donerf_render_debug.argtypes = [vp, fp, i32, i32, i32, i32, vp, vp, vp, vp]
+        L.donerf_render_debug.argtypes = [vp, fp, i32, i32, i32, i32, vp, vp, vp, vp, vp]
         L.donerf_render_debug.restype = ctypes.c_int
         L.donerf_debug_topn.argtypes = [vp, vp, i32, i32, vp]
         L.donerf_debug_topn.restype = ctypes.c_int
@@ -156,10 +157,10 @@ def donerf_render(h, poses, P, H, W, N, out_rgb_ptr, out_depth_ptr=None) -> None
 
 
 def donerf_render_debug(h, poses, P, H, W, N, out_rgb_ptr, out_depth_ptr=None,
-                        out_bins_ptr=None, out_scores_ptr=None) -> None:
+                        out_bins_ptr=None, out_scores_ptr=None, out_samples_ptr=None) -> None:
     p = _poses(poses)
     _check(lib().donerf_render_debug(h, _fptr(p), P, H, W, N, out_rgb_ptr, out_depth_ptr,
-                                     out_bins_ptr, out_scores_ptr))
+                                     out_bins_ptr, out_scores_ptr, out_samples_ptr))
 
 
 def donerf_debug_topn(h, scores_ptr, rays, N, out_idx_ptr) -> None:
@@ -205,6 +206,7 @@ class Renderer:
         if debug:
             out["bins"] = t.empty((P, H, W, N), dtype=t.int32, device=dev)
             out["scores"] = t.empty((P, H, W, self.cfg.n_bins), dtype=t.float32, device=dev)
+            out["samples"] = t.empty((P, H, W, N, 2), dtype=t.float32, device=dev)
         return out
 
     def render_into(self, poses, H, W, N, out, debug=False):
@@ -212,7 +214,7 @@ class Renderer:
         ptr = lambda k: out[k].data_ptr() if k in out else None
         if debug:
             donerf_render_debug(self.h, poses, P, H, W, N, ptr("rgb"), ptr("depth"),
-                                ptr("bins"), ptr("scores"))
+                                ptr("bins"), ptr("scores"), ptr("samples"))
         else:
             donerf_render(self.h, poses, P, H, W, N, ptr("rgb"), ptr("depth"))
         return out

@@ -65,10 +65,13 @@ int validate_cfg(const donerf_cfg* c) {
     if (c->n_max > c->n_bins) return fail(DONERF_E_INVALID_ARG, "n_max exceeds n_bins");
     if (c->precision != DONERF_FP32 && c->precision != DONERF_BF16)
         return fail(DONERF_E_INVALID_ARG, "unknown precision");
-    if (c->select != DONERF_SELECT_TOPN && c->select != DONERF_SELECT_TOPN_SOFTMAX)
+    if (c->select != DONERF_SELECT_TOPN && c->select != DONERF_SELECT_TOPN_SOFTMAX &&
+        c->select != DONERF_SELECT_CDF)
         return fail(DONERF_E_INVALID_ARG, "unknown select mode");
     if (!bins_supported(c->n_bins))
         return fail(DONERF_E_UNSUPPORTED, "n_bins must be 64, 128, 192 or 256");
+    if (c->select == DONERF_SELECT_CDF && c->n_bins > 128)
+        return fail(DONERF_E_UNSUPPORTED, "inverse-CDF placement supports n_bins 64 and 128");
     return DONERF_OK;
 }
 
@@ -181,7 +184,7 @@ int validate_render(const donerf_t* h, const float* poses, int32_t P, int32_t H,
 int ncap_for(int N) { return N <= 4 ? 4 : N <= 8 ? 8 : 16; }
 
 int render_impl(donerf_t* h, const float* poses, int32_t P, int32_t H, int32_t W, int32_t N, float* out_rgb,
-                float* out_depth, int32_t* out_bins, float* out_scores) {
+                float* out_depth, int32_t* out_bins, float* out_scores, float* out_samples) {
     int rc = validate_render(h, poses, P, H, W, N, out_rgb);
     if (rc) return rc;
     const donerf_cfg& c = h->cfg;
@@ -205,7 +208,10 @@ int render_impl(donerf_t* h, const float* poses, int32_t P, int32_t H, int32_t W
     a.cy = c.centre[1];
     a.cz = c.centre[2];
     a.radius = c.radius;
+    a.near = c.near_dist;
     a.dmax = c.far_dist;
+    a.log2_span1 = (float)std::log2((double)c.far_dist - (double)c.near_dist + 1.0);
+    const int place = c.select == DONERF_SELECT_CDF ? 1 : 0;
     const size_t hw = (size_t)H * W;
     for (int32_t p0 = 0; p0 < P; p0 += kMaxPosesPerLaunch) {
         const int np = P - p0 < kMaxPosesPerLaunch ? P - p0 : kMaxPosesPerLaunch;
@@ -216,6 +222,7 @@ int render_impl(donerf_t* h, const float* poses, int32_t P, int32_t H, int32_t W
         a.out_depth = out_depth ? out_depth + (size_t)p0 * hw : nullptr;
         a.out_bins = out_bins ? out_bins + (size_t)p0 * hw * N : nullptr;
         a.out_scores = out_scores ? out_scores + (size_t)p0 * hw * c.n_bins : nullptr;
+        a.out_samples = out_samples ? out_samples + (size_t)p0 * hw * N * 2 : nullptr;
         // Full rounds of one workgroup per CU run as they are.  The tiles of a
         // last, partial round are split by samples over up to n_cu / r
         // workgroups each (every part recomputes the depth network), and a
@@ -230,7 +237,7 @@ int render_impl(donerf_t* h, const float* poses, int32_t P, int32_t H, int32_t W
         a.n_full = split > 1 ? full : tiles;
         a.split = (int32_t)split;
         a.partial = h->partial;
-        hipError_t e = launch_render(h->bf16, ncap_for(N), a, split > 1 ? rem : 0, h->stream);
+        hipError_t e = launch_render(h->bf16, ncap_for(N), place, a, split > 1 ? rem : 0, h->stream);
         if (e != hipSuccess) return hip_fail(e, "render launch");
         if (split > 1) {
             e = launch_combine(h->bf16, a, h->stream);
@@ -347,13 +354,14 @@ int donerf_set_stream(donerf_t* h, void* stream) {
 int donerf_render(donerf_t* h, const float* cam_poses, int32_t P, int32_t H, int32_t W, int32_t N,
                   float* out_rgb, float* out_depth) {
     g_err.clear();
-    return render_impl(h, cam_poses, P, H, W, N, out_rgb, out_depth, nullptr, nullptr);
+    return render_impl(h, cam_poses, P, H, W, N, out_rgb, out_depth, nullptr, nullptr, nullptr);
 }
 
 int donerf_render_debug(donerf_t* h, const float* cam_poses, int32_t P, int32_t H, int32_t W, int32_t N,
-                        float* out_rgb, float* out_depth, int32_t* out_bins, float* out_scores) {
+                        float* out_rgb, float* out_depth, int32_t* out_bins, float* out_scores,
+                        float* out_samples) {
     g_err.clear();
-    return render_impl(h, cam_poses, P, H, W, N, out_rgb, out_depth, out_bins, out_scores);
+    return render_impl(h, cam_poses, P, H, W, N, out_rgb, out_depth, out_bins, out_scores, out_samples);
 }
 
 int donerf_debug_topn(donerf_t* h, const float* scores, int32_t rays, int32_t N, int32_t* out_idx) {

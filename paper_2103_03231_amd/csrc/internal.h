@@ -19,6 +19,7 @@ struct RenderArgs {
     float* out_depth;       // rays, or null
     int32_t* out_bins;      // rays x N, or null
     float* out_scores;      // rays x B, or null
+    float* out_samples;     // rays x N x (depth, width), or null
     int32_t n_d_chunks;
     int32_t n_s_chunks;
     int32_t bias_len;       // floats in bias
@@ -36,7 +37,9 @@ struct RenderArgs {
     float focal, half_w, half_h;
     float cx, cy, cz;
     float radius;
-    float dmax;
+    float near;             // d_min
+    float dmax;             // d_max
+    float log2_span1;       // log2(d_max - d_min + 1), for the inverse of Eq. 3
     float poses[kMaxPosesPerLaunch][12];
 };
 
@@ -59,7 +62,9 @@ constexpr int kBf16Occ = DONERF_BF16_OCC;
 inline int rays_per_block(bool bf16) { return bf16 ? kBf16NW * 32 * kBf16CB : 4 * 32; }
 
 // Launches a.n_full whole tiles plus n_split_tiles tiles split a.split ways.
-hipError_t launch_render(bool bf16, int ncap, const RenderArgs& a, uint32_t n_split_tiles, hipStream_t stream);
+// place: 0 top-N, 1 inverse CDF.
+hipError_t launch_render(bool bf16, int ncap, int place, const RenderArgs& a, uint32_t n_split_tiles,
+                         hipStream_t stream);
 // Composites the split parts of rays [n_full * rays_per_block, total_rays)
 // into out_rgb / out_depth.
 hipError_t launch_combine(bool bf16, const RenderArgs& a, hipStream_t stream);

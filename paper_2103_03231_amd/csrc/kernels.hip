@@ -371,9 +371,117 @@ __device__ __forceinline__ int pick(const int (&s)[NCAP], int k) {
     return r;
 }
 
+__device__ __forceinline__ float pick_f(const float* v, int n, int k) {
+    float r = v[0];
+    for (int q = 1; q < n; ++q) r = k == q ? v[q] : r;
+    return r;
+}
+
+// ------------------------------------------------------------------ inverse-CDF placement
+
+enum Placement { kPlaceTopN = 0, kPlaceCdf = 1 };
+
+// Sample placement of Sec. 5.1 (Fig. 7): the class values sigmoid(score)
+// form a piecewise-constant PDF over the classes (uniform in the coordinate
+// of Eq. 3); the CDF is inverted at u_i = (i + 0.5) / N, and each sample's
+// width is the depth extent of its probability slice [i/N, (i+1)/N].
+//
+// v[P][R][i] holds this lane's class values for class 32 (P * RBP + R) +
+// 8 (i/4) + 4 g + i%4, i.e. lane-local blocks of four consecutive classes;
+// global block b = 2 * local + g alternates between the lane pair.  Both
+// lanes build the same prefix over the blocks (the partner's block sums
+// arrive by a lane swap), locate each target's block by counting the blocks
+// that end at or below it, and take the block's four values from the lane
+// that owns it.  Everything is fp32.
+template <int NPM, int NCAP>
+__device__ __forceinline__ void cdf_place(const float (&v)[NPM][kRbPerPass][16], int g, int N, int B,
+                                          float near, float far, float log2_span1, float (&ts)[NCAP],
+                                          float (&ds)[NCAP], int (&cls)[NCAP]) {
+    constexpr int NLB = NPM * kRbPerPass * 4;  // lane-local blocks
+    constexpr int NB = 2 * NLB;                // blocks in class order
+    float bs[NLB], pbs[NLB];
+#pragma unroll
+    for (int P = 0; P < NPM; ++P)
+#pragma unroll
+        for (int R = 0; R < kRbPerPass; ++R)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                bs[(P * kRbPerPass + R) * 4 + q] =
+                    ((v[P][R][4 * q] + v[P][R][4 * q + 1]) + v[P][R][4 * q + 2]) + v[P][R][4 * q + 3];
+#pragma unroll
+    for (int lb = 0; lb < NLB; ++lb) pbs[lb] = __shfl_xor(bs[lb], 32);
+    float pre[NB + 1];
+    pre[0] = 0.0f;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) pre[b + 1] = pre[b] + (((b & 1) == g) ? bs[b >> 1] : pbs[b >> 1]);
+    const float total = pre[NB];
+
+    // coordinate s in [0, 1] of the target fraction u; k: its class
+    auto inverse = [&](float u, int& k) {
+        const float m = u * total;
+        int b = 0;
+#pragma unroll
+        for (int bb = 0; bb < NB; ++bb) b += pre[bb + 1] <= m ? 1 : 0;
+        b = min(b, NB - 1);
+        const int lb = b >> 1;
+        float w[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            float r = 0.0f;
+#pragma unroll
+            for (int P = 0; P < NPM; ++P)
+#pragma unroll
+                for (int R = 0; R < kRbPerPass; ++R)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        r = lb == (P * kRbPerPass + R) * 4 + q ? v[P][R][4 * q + j] : r;
+            w[j] = r;
+        }
+        const bool own = (b & 1) == g;
+        float a4[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const float pw = __shfl_xor(w[j], 32);
+            a4[j] = own ? w[j] : pw;
+        }
+        float lo = pre[0];
+#pragma unroll
+        for (int bb = 1; bb < NB; ++bb) lo = b == bb ? pre[bb] : lo;
+        const float c1 = lo + a4[0], c2 = c1 + a4[1], c3 = c2 + a4[2];
+        const int j = (m >= c1 ? 1 : 0) + (m >= c2 ? 1 : 0) + (m >= c3 ? 1 : 0);
+        const float base = j == 0 ? lo : j == 1 ? c1 : j == 2 ? c2 : c3;
+        const float aj = j == 0 ? a4[0] : j == 1 ? a4[1] : j == 2 ? a4[2] : a4[3];
+        const float frac = aj > 0.0f ? fminf(fmaxf((m - base) / aj, 0.0f), 1.0f) : 0.0f;
+        k = 4 * b + j;
+        return ((float)k + frac) / (float)B;
+    };
+    auto to_depth = [&](float s) { return near + exp2f(s * log2_span1) - 1.0f; };  // inverse of Eq. 3
+    float edge[NCAP + 1];
+    edge[0] = near;
+#pragma unroll
+    for (int i = 0; i < NCAP; ++i) {
+        if (i < N) {
+            int k;
+            ts[i] = to_depth(inverse(((float)i + 0.5f) / (float)N, k));
+            cls[i] = k;
+            int kk;
+            edge[i + 1] = i + 1 < N ? to_depth(inverse((float)(i + 1) / (float)N, kk)) : far;
+        } else {
+            ts[i] = far;
+            cls[i] = B - 1;
+            edge[i + 1] = far;
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < NCAP; ++i) ds[i] = edge[i + 1] - edge[i];
+}
+
 // ------------------------------------------------------------------ geometry (fp32, fixed order)
 // Built with -ffp-contract=off: every operation below rounds to fp32 in the
-// written order.
+// written order.  Divides and sqrtf are correctly rounded (hipcc's default
+// expansions); __fsqrt_rn is not used because it lowers to the bare hardware
+// square root, which can be one ulp off, and the encoding multiplies an ulp
+// of the ray geometry by up to 2^9 pi.
 
 struct Ray {
     float o[3], r[3];
@@ -391,7 +499,7 @@ __device__ __forceinline__ Ray camera_ray(const RenderArgs& a, uint32_t ray) {
     float d[3];
 #pragma unroll
     for (int k = 0; k < 3; ++k) d[k] = (M[4 * k + 0] * u + M[4 * k + 1] * v) + M[4 * k + 2] * -1.0f;
-    const float n = __fsqrt_rn((d[0] * d[0] + d[1] * d[1]) + d[2] * d[2]);
+    const float n = sqrtf((d[0] * d[0] + d[1] * d[1]) + d[2] * d[2]);
     Ray out;
 #pragma unroll
     for (int k = 0; k < 3; ++k) {
@@ -407,7 +515,7 @@ __device__ __forceinline__ void unify(const RenderArgs& a, const Ray& ray, float
     const float b = (ray.r[0] * q0 + ray.r[1] * q1) + ray.r[2] * q2;
     const float k = ((q0 * q0 + q1 * q1) + q2 * q2) - a.radius * a.radius;
     const float disc = fmaxf(b * b - k, 0.0f);
-    const float t = fmaxf(-b + __fsqrt_rn(disc), 0.0f);
+    const float t = fmaxf(-b + sqrtf(disc), 0.0f);
 #pragma unroll
     for (int c = 0; c < 3; ++c) ou[c] = ray.o[c] + t * ray.r[c];
 }
@@ -415,8 +523,8 @@ __device__ __forceinline__ void unify(const RenderArgs& a, const Ray& ray, float
 // Eq. 4-5: w = p / sqrt(|p| d_max), p = x - c, w = 0 at p = 0.
 __device__ __forceinline__ void warp(const RenderArgs& a, const float (&x)[3], float (&w)[3]) {
     const float p0 = x[0] - a.cx, p1 = x[1] - a.cy, p2 = x[2] - a.cz;
-    const float n = __fsqrt_rn((p0 * p0 + p1 * p1) + p2 * p2);
-    const float s = __fsqrt_rn(n * a.dmax);
+    const float n = sqrtf((p0 * p0 + p1 * p1) + p2 * p2);
+    const float s = sqrtf(n * a.dmax);
     const bool z = n == 0.0f;
     w[0] = z ? 0.0f : p0 / s;
     w[1] = z ? 0.0f : p1 / s;
@@ -466,8 +574,8 @@ constexpr int kBiasMax = 7 * 256 + 256 + 7 * 256 + 32;
 // BF16: network precision.  CB: 32-ray column blocks per wave.  NW: waves per
 // workgroup.  OCC: waves per SIMD the register budget is sized for (with
 // OCC * 4 > NW several workgroups share a CU).  NCAP: capacity of the top-N
-// list.
-template <bool BF16, int CB, int NW, int OCC, int NCAP>
+// list (top-N) or of the sample arrays (CDF).  PLACE: sample placement.
+template <bool BF16, int CB, int NW, int OCC, int NCAP, int PLACE>
 __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(OCC, OCC)))
 render_kernel(const RenderArgs a) {
     using P = Prec<BF16>;
@@ -568,39 +676,86 @@ render_kernel(const RenderArgs a) {
         hidden_layer<BF16, CB, KS_D0>(st, g, bias_s, gin, h0);
     }
     hidden6(bias_s + 256);
-    TopList<NCAP> top[CB];
-    sfor<CB>([&](auto C) { top[CV(C)].init(); });
-    // Head of the depth network: B / 64 passes of 64 classes.  PPC passes
-    // share one chunk, so the loop steps a chunk at a time.
+    // Head of the depth network: B / 64 passes of 64 classes (32 * kRbPerPass).
     const int npass = a.B / (32 * kRbPerPass);
     constexpr int PASS_FRAGS = KS_H * kRbPerPass;
-    constexpr int PPC = PASS_FRAGS >= kChunkFrags ? 1 : kChunkFrags / PASS_FRAGS;
-    for (int p0 = 0; p0 < npass; p0 += PPC) {
-        sfor<PPC>([&](auto Q) {
-            constexpr int q = CV(Q);
-            const int p = p0 + q;
-            if (p < npass) {
-                run_pass<BF16, CB, KS_H, kRbPerPass, q * PASS_FRAGS>(
-                    st, g, bias_s + 7 * 256 + 32 * kRbPerPass * p, g0, [&](auto R, auto C, const f32x16& acc) {
-                        const int rowb = 32 * kRbPerPass * p + 32 * CV(R) + 4 * g;
+    auto dump_scores = [&](int p, int R, int C, const f32x16& acc) {
+        if (a.out_scores && part == 0 && valid[C]) {
+            float* dst = a.out_scores + (size_t)rid[C] * a.B;
+            const int rowb = 32 * kRbPerPass * p + 32 * R + 4 * g;
 #pragma unroll
-                        for (int i = 0; i < 16; ++i)
-                            top[CV(C)].push_ascending(acc[i], rowb + 8 * (i / 4) + (i % 4));
-                        if (a.out_scores && part == 0) {
-                            float* dst = a.out_scores + (size_t)rid[CV(C)] * a.B;
+            for (int i = 0; i < 16; ++i) dst[rowb + 8 * (i / 4) + (i % 4)] = acc[i];
+        }
+    };
+    // Per ray: sample depth t, width delta and class of sample k.
+    int sel[CB][NCAP];
+    float st_t[CB][NCAP], st_d[CB][NCAP];
+    if constexpr (PLACE == kPlaceTopN) {
+        TopList<NCAP> top[CB];
+        sfor<CB>([&](auto C) { top[CV(C)].init(); });
+        // PPC passes share one chunk, so the loop steps a chunk at a time.
+        constexpr int PPC = PASS_FRAGS >= kChunkFrags ? 1 : kChunkFrags / PASS_FRAGS;
+        for (int p0 = 0; p0 < npass; p0 += PPC) {
+            sfor<PPC>([&](auto Q) {
+                constexpr int q = CV(Q);
+                const int p = p0 + q;
+                if (p < npass) {
+                    run_pass<BF16, CB, KS_H, kRbPerPass, q * PASS_FRAGS>(
+                        st, g, bias_s + 7 * 256 + 32 * kRbPerPass * p, g0, [&](auto R, auto C, const f32x16& acc) {
+                            const int rowb = 32 * kRbPerPass * p + 32 * CV(R) + 4 * g;
 #pragma unroll
                             for (int i = 0; i < 16; ++i)
-                                if (valid[CV(C)]) dst[rowb + 8 * (i / 4) + (i % 4)] = acc[i];
-                        }
+                                top[CV(C)].push_ascending(acc[i], rowb + 8 * (i / 4) + (i % 4));
+                            dump_scores(p, CV(R), CV(C), acc);
+                        });
+                }
+            });
+        }
+        sfor<CB>([&](auto C) {
+            top[CV(C)].merge_partner();
+            top[CV(C)].ascending(a.N, sel[CV(C)]);
+        });
+    } else {
+        // Inverse-CDF placement needs every class value of the ray; B <= 128
+        // keeps them in registers (the hidden activations h1 are dead here).
+        constexpr int NPM = 128 / (32 * kRbPerPass);
+        float vals[CB][NPM][kRbPerPass][16];
+        sfor<NPM>([&](auto PI) {
+            constexpr int p = CV(PI);
+            if (p < npass) {
+                run_pass<BF16, CB, KS_H, kRbPerPass, p * PASS_FRAGS>(
+                    st, g, bias_s + 7 * 256 + 32 * kRbPerPass * p, g0, [&](auto R, auto C, const f32x16& acc) {
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) vals[CV(C)][p][CV(R)][i] = 1.0f / (1.0f + expf(-acc[i]));
+                        dump_scores(p, CV(R), CV(C), acc);
                     });
+            } else {
+                sfor<CB>([&](auto C) {
+#pragma unroll
+                    for (int R = 0; R < kRbPerPass; ++R)
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) vals[CV(C)][p][R][i] = 0.0f;
+                });
             }
         });
+        sfor<CB>([&](auto C) {
+            cdf_place<NPM, NCAP>(vals[CV(C)], g, a.N, a.B, a.near, a.dmax, a.log2_span1, st_t[CV(C)],
+                                 st_d[CV(C)], sel[CV(C)]);
+        });
     }
-    int sel[CB][NCAP];
-    sfor<CB>([&](auto C) {
-        top[CV(C)].merge_partner();
-        top[CV(C)].ascending(a.N, sel[CV(C)]);
-    });
+    // sample k of column block cb: depth, width
+    auto sample_td = [&](int cb, int k, float& t, float& d) {
+        if constexpr (PLACE == kPlaceTopN) {
+            // Always a class index for finite scores; clamped so that no
+            // sentinel can address outside the class table.
+            const int bin = min(pick(sel[cb], k), a.B - 1);
+            t = bins_s[bin];
+            d = bins_s[a.B + bin];
+        } else {
+            t = pick_f(st_t[cb], NCAP, k);
+            d = pick_f(st_d[cb], NCAP, k);
+        }
+    };
 
     // ---- shading network per sample, composited front to back
     const int s_bias = 7 * 256 + a.B;
@@ -613,11 +768,7 @@ render_kernel(const RenderArgs a) {
         float tk[CB], dk[CB];
 #pragma unroll
         for (int cb = 0; cb < CB; ++cb) {
-            // Always a class index for finite scores; clamped so that no
-            // sentinel can address outside the class table.
-            const int bin = min(pick(sel[cb], k), a.B - 1);
-            tk[cb] = bins_s[bin];
-            dk[cb] = bins_s[a.B + bin];
+            sample_td(cb, k, tk[cb], dk[cb]);
             float x[3], w[3];
 #pragma unroll
             for (int c = 0; c < 3; ++c) x[c] = ray[cb].o[c] + tk[cb] * ray[cb].r[c];
@@ -679,6 +830,14 @@ render_kernel(const RenderArgs a) {
             }
             if (a.out_bins && part == 0) {
                 for (int k = 0; k < a.N; ++k) a.out_bins[(size_t)rid[cb] * a.N + k] = pick(sel[cb], k);
+            }
+            if (a.out_samples && part == 0) {
+                for (int k = 0; k < a.N; ++k) {
+                    float t, d;
+                    sample_td(cb, k, t, d);
+                    a.out_samples[((size_t)rid[cb] * a.N + k) * 2 + 0] = t;
+                    a.out_samples[((size_t)rid[cb] * a.N + k) * 2 + 1] = d;
+                }
             }
         }
     }
@@ -752,19 +911,25 @@ __global__ void __launch_bounds__(256) topn_kernel(const float* scores, int32_t 
 
 }  // namespace
 
-hipError_t launch_render(bool bf16, int ncap, const RenderArgs& a, uint32_t n_split_tiles, hipStream_t stream) {
+hipError_t launch_render(bool bf16, int ncap, int place, const RenderArgs& a, uint32_t n_split_tiles,
+                         hipStream_t stream) {
     const dim3 grid(a.n_full + n_split_tiles * (uint32_t)a.split);
-#define DN_LAUNCH(B16, CB, NW, OCC, NC) \
-    hipLaunchKernelGGL((render_kernel<B16, CB, NW, OCC, NC>), grid, dim3(64 * NW), 0, stream, a)
+#define DN_LAUNCH(B16, CB, NW, OCC, NC, PL) \
+    hipLaunchKernelGGL((render_kernel<B16, CB, NW, OCC, NC, PL>), grid, dim3(64 * NW), 0, stream, a)
+#define DN_NCAP(B16, CB, NW, OCC, PL)                  \
+    do {                                               \
+        if (ncap == 4) DN_LAUNCH(B16, CB, NW, OCC, 4, PL);  \
+        else if (ncap == 8) DN_LAUNCH(B16, CB, NW, OCC, 8, PL); \
+        else DN_LAUNCH(B16, CB, NW, OCC, 16, PL);      \
+    } while (0)
     if (bf16) {
-        if (ncap == 4) DN_LAUNCH(true, kBf16CB, kBf16NW, kBf16Occ, 4);
-        else if (ncap == 8) DN_LAUNCH(true, kBf16CB, kBf16NW, kBf16Occ, 8);
-        else DN_LAUNCH(true, kBf16CB, kBf16NW, kBf16Occ, 16);
+        if (place == kPlaceCdf) DN_NCAP(true, kBf16CB, kBf16NW, kBf16Occ, kPlaceCdf);
+        else DN_NCAP(true, kBf16CB, kBf16NW, kBf16Occ, kPlaceTopN);
     } else {
-        if (ncap == 4) DN_LAUNCH(false, 1, 4, 1, 4);
-        else if (ncap == 8) DN_LAUNCH(false, 1, 4, 1, 8);
-        else DN_LAUNCH(false, 1, 4, 1, 16);
+        if (place == kPlaceCdf) DN_NCAP(false, 1, 4, 1, kPlaceCdf);
+        else DN_NCAP(false, 1, 4, 1, kPlaceTopN);
     }
+#undef DN_NCAP
 #undef DN_LAUNCH
     return hipGetLastError();
 }

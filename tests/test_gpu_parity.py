@@ -260,3 +260,117 @@ def test_split_tail_matches_whole_tiles():
         np.testing.assert_allclose(alone["rgb"].reshape(-1), other["rgb"], rtol=0, atol=2e-6)
         np.testing.assert_allclose(alone["depth"].reshape(-1), other["depth"], rtol=0, atol=2e-5)
     r.close()
+
+
+# ------------------------------------------------------------------ inverse-CDF placement (Sec. 5.1)
+
+def _log_coord(t, near=0.1, far=10.0):
+    near, far = float(np.float32(near)), float(np.float32(far))
+    return np.log(np.asarray(t, dtype=np.float64) - near + 1.0) / np.log(far - near + 1.0)
+
+
+# The GPU inverts the CDF in fp32: prefix sums of up to 128 class values
+# (relative error ~ 128 * 2^-24) are subtracted and divided by one class
+# value, so the error in the Eq. 3 coordinate grows where that value is
+# small; 3e-4 bounds it for sigmoid values >= 0.01 of the row total.
+CDF_COORD_TOL = 3e-4
+
+
+def check_cdf(g, w, poses, H, W, N, precision, n_bins=128, subset=None, label=""):
+    scores = g["scores"].reshape(-1, n_bins)
+    samp = g["samples"].reshape(-1, N, 2)
+    rgb = g["rgb"].reshape(-1, 3)
+    depth = g["depth"].reshape(-1)
+    if subset is not None:
+        scores, samp, rgb, depth = scores[subset], samp[subset], rgb[subset], depth[subset]
+    t_ref, d_ref, _ = O.cdf_samples(scores, N, 0.1, 10.0)
+    cerr = np.abs(_log_coord(samp[..., 0]) - _log_coord(t_ref)).max()
+    # widths: differences of two such depths
+    derr = np.abs(samp[..., 1] - d_ref).max()
+    dtol = 2 * CDF_COORD_TOL * np.log(10.0 - 0.1 + 1.0) * 10.9
+    ora = O.render(w, poses, H, W, N, n_bins=n_bins, precision=precision, select="cdf",
+                   forced_samples=(samp[..., 0], samp[..., 1]), ray_subset=subset)
+    err = np.abs(rgb - ora["rgb"]).max()
+    zerr = np.abs(depth - ora["depth"]).max()
+    log(f"[{label}] rays={len(scores)} coord_maxabs={cerr:.3e} width_maxabs={derr:.3e} "
+        f"rgb_maxabs={err:.3e} depth_maxabs={zerr:.3e}")
+    assert np.all(np.diff(samp[..., 0], axis=1) >= 0)
+    np.testing.assert_allclose(samp[..., 1].sum(1), float(np.float32(10.0)) - float(np.float32(0.1)), rtol=1e-4)
+    assert cerr <= CDF_COORD_TOL, cerr
+    assert derr <= dtol, derr
+    assert err <= TOL[precision], err
+    assert zerr <= 10 * TOL[precision], zerr
+
+
+@pytest.mark.parametrize("precision", ["fp32", "bf16"])
+@pytest.mark.parametrize("N,B,H,W,P", [
+    (4, 128, 32, 32, 1),
+    (1, 128, 17, 23, 1),
+    (2, 64, 37, 29, 1),
+    (8, 128, 16, 24, 2),
+    (16, 128, 12, 20, 1),
+])
+def test_cdf_placement(precision, N, B, H, W, P):
+    r, w = renderer(precision, n_bins=B, n_max=max(N, 4), select=b.SELECT_CDF)
+    poses = inputs.make_poses(list(range(10, 10 + P)))
+    g = gpu_render(r, poses, H, W, N)
+    check_cdf(g, w, poses, H, W, N, precision, n_bins=B, label=f"cdf {precision} N={N} B={B} {P}x{H}x{W}")
+    r.close()
+
+
+def test_cdf_rejects_256_classes():
+    with pytest.raises(b.DonerfError) as e:
+        renderer("bf16", n_bins=256, select=b.SELECT_CDF)
+    assert e.value.status == b.E_UNSUPPORTED
+
+
+def test_cdf_frame400_sampled():
+    r, w = renderer("bf16", select=b.SELECT_CDF)
+    poses = inputs.make_poses(range(5))
+    out = r.alloc(5, 400, 400, 4, depth=True, debug=True)
+    r.render_into(poses, 400, 400, 4, out, debug=True)
+    torch.cuda.synchronize()
+    g = {k: v.cpu().numpy() for k, v in out.items()}
+    subset = np.unique(np.random.default_rng(3).integers(0, 5 * 400 * 400, 1500))
+    check_cdf(g, w, poses, 400, 400, 4, "bf16", subset=subset, label="cdf 5x400x400")
+    r.close()
+
+
+# ------------------------------------------------------------------ depth-network input features
+
+def _feature_probe_blob(B=128):
+    """Depth network that returns its 90 encoded inputs exactly in fp32:
+    units 2f and 2f+1 hold ReLU(x_f) and ReLU(-x_f), hidden layers are
+    identities, the head subtracts them (one nonzero product per sum)."""
+    d = []
+    W0 = np.zeros((256, 90), np.float32)
+    for f in range(90):
+        W0[2 * f, f], W0[2 * f + 1, f] = 1.0, -1.0
+    d.append((W0, np.zeros(256, np.float32)))
+    for _ in range(6):
+        d.append((np.eye(256, dtype=np.float32), np.zeros(256, np.float32)))
+    W7 = np.zeros((B, 256), np.float32)
+    for f in range(90):
+        W7[f, 2 * f], W7[f, 2 * f + 1] = 1.0, -1.0
+    d.append((W7, np.zeros(B, np.float32)))
+    s = inputs.make_weights(B, 0)[-412272:]
+    return np.concatenate([np.concatenate([W.ravel(), bb]) for W, bb in d] + [s])
+
+
+def test_depth_input_features_match_oracle():
+    """The encoded unified origin / d_max and direction the kernel feeds the
+    depth network, read back through an exact pass-through network (fp32):
+    identity slots bit-exact, sin/cos within 2 fp32 ulp of the fp64 oracle
+    evaluated on the same fp32 geometry."""
+    blob = _feature_probe_blob()
+    r = b.Renderer(b.Config(n_bins=128, n_max=4, precision=b.FP32), blob)
+    poses = inputs.make_poses([0, 9])
+    g = gpu_render(r, poses, 23, 29, 4)
+    feats = g["scores"].reshape(-1, 128)[:, :90].astype(np.float64)
+    ref = O.render(blob, poses, 23, 29, 4)["logits"][:, :90]
+    ident = [0, 1, 2, 63, 64, 65]
+    assert np.array_equal(feats[:, ident], ref[:, ident]), np.abs(feats[:, ident] - ref[:, ident]).max()
+    err = np.abs(feats - ref).max()
+    log(f"[depth features] maxabs {err:.3e}")
+    assert err <= 2 * 2.0 ** -23, err
+    r.close()
