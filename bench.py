@@ -31,8 +31,8 @@ HBM_PEAK_GBS = 8000.0
 # render_kernel_frame400_n4_bf16_traffic.md) scaled by the same counters on a
 # plain 256 MiB copy (FETCH_SIZE reads half the bytes moved: x2; WRITE_SIZE
 # exact: x1).  Valid only for the kernel sources they were taken on.
-MEASURED_TRAFFIC = {"sources_sha256_16": "9ff151d5d842dbc3", "workload": "frame400_n4_bf16",
-                    "fetch_kib": 7330.8 * 2, "write_kib": 11760.0}
+MEASURED_TRAFFIC = {"sources_sha256_16": "21c89448c12e560c", "workload": "frame400_n4_bf16",
+                    "fetch_kib": 7332.5 * 2, "write_kib": 11760.0}
 KERNEL_SOURCES = ("paper_2103_03231_amd/csrc/kernels.hip", "paper_2103_03231_amd/csrc/layout.h",
                   "paper_2103_03231_amd/csrc/internal.h")
 
@@ -77,7 +77,7 @@ def cpu_baseline(wl, weights, poses, n_sample):
     log(f"cpu baseline: oracle ({wl.precision}) on {len(sub)} sampled rays")
     t0 = time.perf_counter()
     O.render(weights, poses, wl.H, wl.W, wl.N, n_bins=wl.n_bins, fov_x_deg=wl.fov_deg,
-             precision=wl.precision, ray_subset=sub)
+             precision=wl.precision, select=wl.select, ray_subset=sub)
     dt = time.perf_counter() - t0
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     return {"value": len(sub) / dt / 1e6, "unit": "Mrays/s", "cores": int(threads), "kind": "oracle",
@@ -127,7 +127,7 @@ def main():
     poses = wl.poses()
     P = len(poses)
     prec = b.BF16 if wl.precision == "bf16" else b.FP32
-    sel = b.SELECT_TOPN_SOFTMAX if wl.select == "topn_softmax" else b.SELECT_TOPN
+    sel = {"topn": b.SELECT_TOPN, "topn_softmax": b.SELECT_TOPN_SOFTMAX, "cdf": b.SELECT_CDF}[wl.select]
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
     r = b.Renderer(b.Config(n_bins=wl.n_bins, n_max=wl.N, precision=prec, fov_x_deg=wl.fov_deg,
@@ -184,13 +184,13 @@ def main():
         "data": "synthetic: seeded cameras on a sphere of radius 1.5 looking at the origin, "
                 "He-uniform random-init weights (SplitMix64 seed 0)",
         "config": {"workload": wl.name, "poses": P, "H": wl.H, "W": wl.W, "samples_per_ray": wl.N,
-                   "depth_classes": wl.n_bins, "rays_per_step": rays,
+                   "depth_classes": wl.n_bins, "placement": wl.select, "rays_per_step": rays,
                    "algorithmic_mflop_per_ray": round(algorithmic_flop_per_ray(wl.N, wl.n_bins) / 1e6, 4),
                    "padded_mflop_per_ray": round(padded_flop_per_ray(wl.N, wl.n_bins) / 1e6, 4)},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(achieved / peak, 4),
                      "traffic": traffic,
-                     "kernel": "render_kernel<bf16>", "kernel_ms": round(avg_kern_ms, 4)},
+                     "kernel": f"render_kernel<{wl.precision}>", "kernel_ms": round(avg_kern_ms, 4)},
     }
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(wl, weights, poses, args.cpu_sample)

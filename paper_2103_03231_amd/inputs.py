@@ -172,7 +172,7 @@ class Workload:
     n_bins: int = 128
     fov_deg: float = 60.0
     precision: str = "bf16"          # 'fp32' or 'bf16'
-    select: str = "topn"              # 'topn' or 'topn_softmax'
+    select: str = "topn"              # 'topn', 'topn_softmax' or 'cdf'
     want_depth: bool = False
     stereo: bool = False
     near: float = 0.1
@@ -198,6 +198,8 @@ class Workload:
 WORKLOADS = {
     "tiny32_fp32": Workload("tiny32_fp32", 32, 32, (0,), 4, precision="fp32"),
     "frame400_n4_bf16": Workload("frame400_n4_bf16", 400, 400, (0, 1, 2, 3, 4), 4),
+    "frame400_n4_cdf_bf16": Workload("frame400_n4_cdf_bf16", 400, 400, (0, 1, 2, 3, 4), 4,
+                                     select="cdf", want_depth=True),
     "frame800_n8_depth_bf16": Workload("frame800_n8_depth_bf16", 800, 800, (0, 1, 2, 3, 4), 8,
                                        want_depth=True),
     "hd1080_n4_softmax_bf16": Workload("hd1080_n4_softmax_bf16", 1080, 1920, tuple(range(10)), 4,

@@ -324,15 +324,17 @@ def test_cdf_rejects_256_classes():
     assert e.value.status == b.E_UNSUPPORTED
 
 
-def test_cdf_frame400_sampled():
-    r, w = renderer("bf16", select=b.SELECT_CDF)
-    poses = inputs.make_poses(range(5))
-    out = r.alloc(5, 400, 400, 4, depth=True, debug=True)
-    r.render_into(poses, 400, 400, 4, out, debug=True)
+def test_frame400_n4_cdf_bf16_sampled():
+    wl = inputs.WORKLOADS["frame400_n4_cdf_bf16"]
+    r, w = renderer(wl.precision, n_bins=wl.n_bins, n_max=wl.N, select=b.SELECT_CDF)
+    poses = wl.poses()
+    P = len(poses)
+    out = r.alloc(P, wl.H, wl.W, wl.N, depth=True, debug=True)
+    r.render_into(poses, wl.H, wl.W, wl.N, out, debug=True)
     torch.cuda.synchronize()
     g = {k: v.cpu().numpy() for k, v in out.items()}
-    subset = np.unique(np.random.default_rng(3).integers(0, 5 * 400 * 400, 1500))
-    check_cdf(g, w, poses, 400, 400, 4, "bf16", subset=subset, label="cdf 5x400x400")
+    subset = np.unique(np.random.default_rng(3).integers(0, P * wl.H * wl.W, 1500))
+    check_cdf(g, w, poses, wl.H, wl.W, wl.N, wl.precision, subset=subset, label=wl.name)
     r.close()
 
 
