@@ -8,7 +8,9 @@ It follows DONeRF (Neff et al., EGSR 2021, arXiv 2103.03231) one step at a time:
 
   ray through a pixel (Sec. 4, Eq. 1)
   -> ray unification onto the view-cell sphere (Sec. 5.2, Fig. 8)
-  -> encoded depth-network input, normalised by d_max (Sec. 4, Eq. 2)
+  -> encoded depth-network input, normalised by d_max (Sec. 4, Eq. 2), or the
+     paper's unencoded input: unified origin, direction and one position per
+     depth-class centre (Sec. 5.2, App. D)
   -> depth-oracle network, 8 linear layers of 256 units (Sec. 5.3, App. D)
   -> log-discretised depth bins (Sec. 4, Eq. 3; Sec. 5.2) and top-N selection
   -> samples x = o + t r (Eq. 1) at the selected bin centres
@@ -22,15 +24,17 @@ fp32 with the operation order written below, so that a fp32 implementation
 with the same order reproduces it bit for bit.  Encodings, matrix products
 (fp64 accumulation) and compositing run in fp64.  In ``precision='bf16'`` the
 oracle rounds to bf16 (round-to-nearest-even) exactly where a bf16 network
-does: weights, encoded features and each hidden activation after bias + ReLU.
+does: weights, encoded features and each hidden activation after bias + ReLU
+(the unencoded positions input is not rounded).
 Values are first rounded to fp32 and then to bf16.  Logits and head outputs
 stay unrounded.
 
 Readings where the paper is silent are listed in the design document; each
 function names the one it uses.
 
-Every function is pinned by ``tests/test_oracle_pins.py`` against closed
-forms, invariants, the paper's Table 2 and brute force on tiny inputs.
+Every function is pinned by ``tests/test_oracle_pins.py`` (and the
+``test_oracle_*.py`` files beside it) against closed forms, invariants, the
+paper's Table 2 and brute force on tiny inputs.
 """
 from __future__ import annotations
 
@@ -175,14 +179,25 @@ def encode(v, L):
 
 # ---------------------------------------------------------------- networks
 
-def split_weights(blob, n_bins):
+def depth_in_dims(n_bins, depth_input="encoded"):
+    """Inputs of the depth network's first layer: 90 for the encoded unified
+    origin and direction, 6 + 3 n_bins for the paper's unencoded input of
+    Sec. 5.2 (unified origin, direction, one position per class centre)."""
+    if depth_input == "encoded":
+        return 3 + 6 * L_POS + 3 + 6 * L_DIR
+    if depth_input == "positions":
+        return 6 + 3 * n_bins
+    raise ValueError(depth_input)
+
+
+def split_weights(blob, n_bins, depth_input="encoded"):
     """Parse the flat fp32 blob (per layer W[out][in] row-major then b[out];
     depth network layers 0..7, then shading network layers 0..7) into two
     lists of (W, b) in fp64.  Shapes follow App. D: 8 layers of 256 units;
-    the depth network maps 90 encoded inputs to n_bins classes; the shading
-    network maps 63 encoded inputs to (r, g, b, sigma) and reads the 27
-    encoded direction values again in its last layer."""
-    dims_in = 3 + 6 * L_POS + 3 + 6 * L_DIR
+    the depth network maps its inputs (``depth_in_dims``) to n_bins classes;
+    the shading network maps 63 encoded inputs to (r, g, b, sigma) and reads
+    the 27 encoded direction values again in its last layer."""
+    dims_in = depth_in_dims(n_bins, depth_input)
     shapes = ([(HIDDEN, dims_in)] + [(HIDDEN, HIDDEN)] * 6 + [(n_bins, HIDDEN)]
               + [(HIDDEN, 3 + 6 * L_POS)] + [(HIDDEN, HIDDEN)] * 6
               + [(4, HIDDEN + 3 + 6 * L_DIR)])
@@ -199,14 +214,14 @@ def split_weights(blob, n_bins):
     return layers[:8], layers[8:]
 
 
-def mlp(layers, x, precision="fp64", skip=None):
+def mlp(layers, x, precision="fp64", skip=None, round_input=True):
     """ReLU MLP: h = ReLU(W_l h + b_l) for every layer but the last, whose
     output is returned without activation.  ``skip`` (rows x s) is appended to
     the last layer's input (App. D's single direction skip).  x is (rows, in).
-    In bf16 mode weights, inputs and hidden activations are rounded to bf16;
-    sums accumulate in fp64."""
+    In bf16 mode weights, inputs (unless ``round_input`` is false) and hidden
+    activations are rounded to bf16; sums accumulate in fp64."""
     rb = round_bf16 if precision == "bf16" else (lambda a: np.asarray(a, dtype=np.float64))
-    h = rb(x)
+    h = rb(x) if round_input else np.asarray(x, dtype=np.float64)
     n = len(layers)
     for li, (W, b) in enumerate(layers):
         if li == n - 1 and skip is not None:
@@ -217,6 +232,23 @@ def mlp(layers, x, precision="fp64", skip=None):
         else:
             h = y
     return h
+
+
+def depth_positions_input(o, r, ou, centre, d_max, centres):
+    """The depth network's input as Sec. 5.2 describes it, without encoding:
+    the unified origin, the ray direction and one 3-D position along the ray
+    at the centre of every depth class, positions and origin moved into the
+    view cell's frame and divided by d_max as in Eq. 2.  The class centres are
+    depths from the camera origin o (Eq. 1), so position k is o + c_k r.
+    fp32 geometry in the written order; returns (n, 6 + 3 B) fp32 in the
+    order [origin xyz, direction xyz, position 0 xyz, position 1 xyz, ...]."""
+    c = np.asarray(centre, dtype=F32)
+    d_max = F32(d_max)
+    cen = np.asarray(centres, dtype=F32)
+    v = ((ou - c) / d_max).astype(F32)
+    x = sample_points(o, r, np.broadcast_to(cen[None, :], (o.shape[0], cen.size))).astype(F32)
+    p = ((x - c) / d_max).astype(F32)
+    return np.concatenate([v, r.astype(F32), p.reshape(o.shape[0], -1)], axis=1)
 
 
 # ---------------------------------------------------------------- selection
@@ -328,21 +360,33 @@ def composite(raw, t, delta):
 # ---------------------------------------------------------------- full path
 
 def render_rays(d_layers, s_layers, o, r, N, near, far, n_bins, centre, radius,
-                precision="fp64", select="topn", forced_bins=None, forced_samples=None):
+                precision="fp64", select="topn", forced_bins=None, forced_samples=None,
+                depth_input="encoded"):
     """Per-ray inference for rays (o, r) (fp32, (n, 3)).  Returns dict with
     rgb (n,3), depth (n,), bins (n,N) int32, logits (n,B) fp64, the sample
     depths t and widths delta (n,N) and, for select='topn_softmax', probs
     (n,B) fp32.  select='cdf' places samples by the inverse CDF (Sec. 5.1).
-    forced_samples = (t, delta) overrides the placement (for comparisons)."""
+    forced_samples = (t, delta) overrides the placement (for comparisons).
+    depth_input='positions' feeds the depth network the paper's unencoded
+    input (``depth_positions_input``); in bf16 mode that input is not
+    rounded (only the weights and hidden activations are)."""
     d_max = F32(far)
     c = np.asarray(centre, dtype=F32)
-    # 1-2: unification and the encoded depth-network input (Eq. 2 / Sec. 5.2).
+    # 1-2: unification and the depth-network input (Eq. 2 / Sec. 5.2).
     ou = unify(o, r, c, radius)
-    v = ((ou - c) / d_max).astype(F32)
     enc_r = encode(r, L_DIR)
-    x0 = np.concatenate([encode(v, L_POS), enc_r], axis=1)
+    if depth_input == "encoded":
+        v = ((ou - c) / d_max).astype(F32)
+        x0 = np.concatenate([encode(v, L_POS), enc_r], axis=1)
+        round_in = True
+    elif depth_input == "positions":
+        _, centres, _ = bin_table(near, far, n_bins)
+        x0 = depth_positions_input(o, r, ou, c, d_max, centres)
+        round_in = False
+    else:
+        raise ValueError(depth_input)
     # 3: depth oracle network -> class scores.
-    logits = mlp(d_layers, x0, precision)
+    logits = mlp(d_layers, x0, precision, round_input=round_in)
     out = {"logits": logits}
     # 4: selection of N classes.
     lg32 = logits.astype(F32)
@@ -381,10 +425,11 @@ def render_rays(d_layers, s_layers, o, r, N, near, far, n_bins, centre, radius,
 
 def render(weights, poses, H, W, N, n_bins=128, near=0.1, far=10.0, fov_x_deg=60.0,
            centre=(0.0, 0.0, 0.0), radius=1.5, precision="fp64", select="topn",
-           forced_bins=None, ray_subset=None, chunk=8192, forced_samples=None):
+           forced_bins=None, ray_subset=None, chunk=8192, forced_samples=None,
+           depth_input="encoded"):
     """Render P poses (P, 3, 4) of H x W rays.  Returns rgb (P*H*W, 3), depth,
     bins and logits for every ray (or for ``ray_subset``, global ray ids)."""
-    d_layers, s_layers = split_weights(weights, n_bins)
+    d_layers, s_layers = split_weights(weights, n_bins, depth_input)
     poses = np.asarray(poses, dtype=F32).reshape(-1, 3, 4)
     hw = H * W
     ids = np.arange(len(poses) * hw) if ray_subset is None else np.asarray(ray_subset, dtype=np.int64)
@@ -403,7 +448,7 @@ def render(weights, poses, H, W, N, n_bins=128, near=0.1, far=10.0, fov_x_deg=60
         part = render_rays(d_layers, s_layers, o[sl], r[sl], N, near, far, n_bins,
                            centre, radius, precision, select,
                            None if fb is None else fb[s:s + chunk],
-                           None if fs is None else (fs[0][sl], fs[1][sl]))
+                           None if fs is None else (fs[0][sl], fs[1][sl]), depth_input)
         for k, val in part.items():
             res.setdefault(k, []).append(val)
     return {k: np.concatenate(v) for k, v in res.items()}

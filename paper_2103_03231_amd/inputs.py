@@ -37,15 +37,22 @@ DIR_SKIP = 27
 S_OUT = 4
 
 
-def layer_shapes(n_bins: int):
+def depth_inputs(n_bins: int, depth_input: str = "encoded") -> int:
+    """Width of the depth network's first layer: 90 encoded inputs, or
+    6 + 3 n_bins for the unencoded origin, direction and class positions."""
+    return {"encoded": D_IN, "positions": 6 + 3 * n_bins}[depth_input]
+
+
+def layer_shapes(n_bins: int, depth_input: str = "encoded"):
     """(out, in) of the 16 linear layers: depth network 0..7, then shading 0..7."""
-    d = [(HIDDEN, D_IN)] + [(HIDDEN, HIDDEN)] * 6 + [(n_bins, HIDDEN)]
+    d = ([(HIDDEN, depth_inputs(n_bins, depth_input))] + [(HIDDEN, HIDDEN)] * 6
+         + [(n_bins, HIDDEN)])
     s = [(HIDDEN, S_IN)] + [(HIDDEN, HIDDEN)] * 6 + [(S_OUT, HIDDEN + DIR_SKIP)]
     return d + s
 
 
-def n_weights(n_bins: int) -> int:
-    return sum(o * i + o for o, i in layer_shapes(n_bins))
+def n_weights(n_bins: int, depth_input: str = "encoded") -> int:
+    return sum(o * i + o for o, i in layer_shapes(n_bins, depth_input))
 
 
 class SplitMix64:
@@ -73,7 +80,7 @@ class SplitMix64:
         return (self.next(n) >> np.uint64(40)).astype(np.float64) * (2.0 ** -24)
 
 
-def make_weights(n_bins: int = 128, seed: int = 0) -> np.ndarray:
+def make_weights(n_bins: int = 128, seed: int = 0, depth_input: str = "encoded") -> np.ndarray:
     """Flat fp32 weight blob: for each layer W[out][in] row-major, then b[out].
 
     W ~ U(-a, a) with a = sqrt(6 / fan_in) (He-uniform), b ~ U(-1/sqrt(fan_in),
@@ -81,13 +88,13 @@ def make_weights(n_bins: int = 128, seed: int = 0) -> np.ndarray:
     blob order from one SplitMix64 stream."""
     rng = SplitMix64(seed)
     parts = []
-    for out_f, in_f in layer_shapes(n_bins):
+    for out_f, in_f in layer_shapes(n_bins, depth_input):
         a = math.sqrt(6.0 / in_f)
         parts.append((a * (2.0 * rng.uniform(out_f * in_f) - 1.0)).astype(np.float32))
         bb = 1.0 / math.sqrt(in_f)
         parts.append((bb * (2.0 * rng.uniform(out_f) - 1.0)).astype(np.float32))
     blob = np.concatenate(parts)
-    assert blob.size == n_weights(n_bins)
+    assert blob.size == n_weights(n_bins, depth_input)
     return blob
 
 
@@ -173,6 +180,7 @@ class Workload:
     fov_deg: float = 60.0
     precision: str = "bf16"          # 'fp32' or 'bf16'
     select: str = "topn"              # 'topn', 'topn_softmax' or 'cdf'
+    depth_input: str = "encoded"      # 'encoded' (90 inputs) or 'positions' (6 + 3 B)
     want_depth: bool = False
     stereo: bool = False
     near: float = 0.1

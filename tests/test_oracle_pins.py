@@ -251,7 +251,8 @@ def test_flops_reproduce_paper_table2():
     for method, n, _storage, mflop in rows:
         n, mflop = int(n), float(mflop)
         if method == "donerf":
-            got = 2 * O.mlp_macs_per_ray(n, n_bins=128, d_in=390) / 1e6
+            # the paper's depth network: the unencoded input of Sec. 5.2
+            got = 2 * O.mlp_macs_per_ray(n, n_bins=128, d_in=O.depth_in_dims(128, "positions")) / 1e6
         else:  # NeRF: n evaluations of the shading-shaped network
             per_eval = O.mlp_macs_per_ray(1) - O.mlp_macs_per_ray(0)
             got = 2 * n * per_eval / 1e6
