@@ -33,8 +33,9 @@ HBM_PEAK_GBS = 8000.0
 # exact: x1).  Valid only for the kernel sources they were taken on.
 MEASURED_TRAFFIC = {"sources_sha256_16": "21c89448c12e560c", "workload": "frame400_n4_bf16",
                     "fetch_kib": 7332.5 * 2, "write_kib": 11760.0}
-KERNEL_SOURCES = ("paper_2103_03231_amd/csrc/kernels.hip", "paper_2103_03231_amd/csrc/layout.h",
-                  "paper_2103_03231_amd/csrc/internal.h")
+# the sources the bf16 top-N render kernel is built from
+KERNEL_SOURCES = ("paper_2103_03231_amd/csrc/render_kernel.h", "paper_2103_03231_amd/csrc/render_bf16_topn.hip",
+                  "paper_2103_03231_amd/csrc/layout.h", "paper_2103_03231_amd/csrc/internal.h")
 
 
 def kernel_sources_sha() -> str:
@@ -46,19 +47,26 @@ def kernel_sources_sha() -> str:
     return h.hexdigest()[:16]
 
 
-def algorithmic_flop_per_ray(N: int, n_bins: int) -> int:
+def depth_in_folded(depth_input: str) -> int:
+    """Inputs of the first depth layer as evaluated: 90 encoded values, or the
+    9 columns the unencoded positions input folds into (its 6 + 3 B inputs
+    are affine in the ray)."""
+    return {"encoded": 90, "positions": 9}[depth_input]
+
+
+def algorithmic_flop_per_ray(N: int, n_bins: int, d_in: int = 90) -> int:
     """2 x multiply-adds of both networks for one ray (8 layers of 256 units):
-    depth network 90->256, 6 x 256->256, 256->B once; shading network
+    depth network d_in->256, 6 x 256->256, 256->B once; shading network
     63->256, 6 x 256->256, 283->4 for each of the N samples."""
-    d = 90 * 256 + 6 * 256 * 256 + 256 * n_bins
+    d = d_in * 256 + 6 * 256 * 256 + 256 * n_bins
     s = 63 * 256 + 6 * 256 * 256 + (256 + 27) * 4
     return 2 * (d + N * s)
 
 
-def padded_flop_per_ray(N: int, n_bins: int) -> int:
-    """2 x multiply-adds the MFMA tiles execute (K padded to 96 / 64 / 288,
-    shading head padded to 32 rows)."""
-    d = 96 * 256 + 6 * 256 * 256 + 256 * n_bins
+def padded_flop_per_ray(N: int, n_bins: int, d_in: int = 90) -> int:
+    """2 x multiply-adds the MFMA tiles execute (K padded to 96 (16 for the
+    folded positions layer) / 64 / 288, shading head padded to 32 rows)."""
+    d = (96 if d_in == 90 else 16) * 256 + 6 * 256 * 256 + 256 * n_bins
     s = 64 * 256 + 6 * 256 * 256 + 288 * 32
     return 2 * (d + N * s)
 
@@ -77,7 +85,7 @@ def cpu_baseline(wl, weights, poses, n_sample):
     log(f"cpu baseline: oracle ({wl.precision}) on {len(sub)} sampled rays")
     t0 = time.perf_counter()
     O.render(weights, poses, wl.H, wl.W, wl.N, n_bins=wl.n_bins, fov_x_deg=wl.fov_deg,
-             precision=wl.precision, select=wl.select, ray_subset=sub)
+             precision=wl.precision, select=wl.select, ray_subset=sub, depth_input=wl.depth_input)
     dt = time.perf_counter() - t0
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     return {"value": len(sub) / dt / 1e6, "unit": "Mrays/s", "cores": int(threads), "kind": "oracle",
@@ -123,15 +131,16 @@ def main():
     from paper_2103_03231_amd import inputs
 
     wl = inputs.WORKLOADS[args.workload]
-    weights = inputs.make_weights(wl.n_bins, 0)
+    weights = inputs.make_weights(wl.n_bins, 0, wl.depth_input)
     poses = wl.poses()
     P = len(poses)
     prec = b.BF16 if wl.precision == "bf16" else b.FP32
     sel = {"topn": b.SELECT_TOPN, "topn_softmax": b.SELECT_TOPN_SOFTMAX, "cdf": b.SELECT_CDF}[wl.select]
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
+    din = {"encoded": b.DEPTH_ENCODED, "positions": b.DEPTH_POSITIONS}[wl.depth_input]
     r = b.Renderer(b.Config(n_bins=wl.n_bins, n_max=wl.N, precision=prec, fov_x_deg=wl.fov_deg,
-                            select=sel), weights)
+                            select=sel, depth_input=din), weights)
     out = r.alloc(P, wl.H, wl.W, wl.N, depth=wl.want_depth)
     log(f"workload {wl.name}: {P} x {wl.H} x {wl.W} rays, N={wl.N}, B={wl.n_bins}, {wl.precision}")
 
@@ -157,7 +166,8 @@ def main():
     rays = wl.rays
     ms_step = wall * 1e3 / args.steps
     value = rays / (ms_step * 1e-3) / 1e6
-    flop_launch = algorithmic_flop_per_ray(wl.N, wl.n_bins) * rays
+    d_in = depth_in_folded(wl.depth_input)
+    flop_launch = algorithmic_flop_per_ray(wl.N, wl.n_bins, d_in) * rays
     achieved = flop_launch / (avg_kern_ms * 1e-3) / 1e12
     peak = MFMA_PEAK_TFLOPS[wl.precision]
     paper_mrays = 400 * 400 / 22e-3 / 1e6   # 22 ms per 400x400 frame, N = 4
@@ -184,9 +194,10 @@ def main():
         "data": "synthetic: seeded cameras on a sphere of radius 1.5 looking at the origin, "
                 "He-uniform random-init weights (SplitMix64 seed 0)",
         "config": {"workload": wl.name, "poses": P, "H": wl.H, "W": wl.W, "samples_per_ray": wl.N,
-                   "depth_classes": wl.n_bins, "placement": wl.select, "rays_per_step": rays,
-                   "algorithmic_mflop_per_ray": round(algorithmic_flop_per_ray(wl.N, wl.n_bins) / 1e6, 4),
-                   "padded_mflop_per_ray": round(padded_flop_per_ray(wl.N, wl.n_bins) / 1e6, 4)},
+                   "depth_classes": wl.n_bins, "placement": wl.select, "depth_input": wl.depth_input,
+                   "rays_per_step": rays,
+                   "algorithmic_mflop_per_ray": round(algorithmic_flop_per_ray(wl.N, wl.n_bins, d_in) / 1e6, 4),
+                   "padded_mflop_per_ray": round(padded_flop_per_ray(wl.N, wl.n_bins, d_in) / 1e6, 4)},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(achieved / peak, 4),
                      "traffic": traffic,

@@ -6,8 +6,9 @@
  * Networks", EGSR 2021).  For every pixel ray (Sec. 4, Eq. 1) it
  *   1. moves the ray origin onto the sphere around the view cell (Sec. 5.2),
  *   2. evaluates the depth-oracle network once on the encoded unified origin
- *      and direction, giving one score per logarithmic depth class (Sec. 5.1,
- *      Eq. 3 discretisation),
+ *      and direction (or on the paper's unencoded input: unified origin,
+ *      direction and one position per class centre, Sec. 5.2), giving one
+ *      score per logarithmic depth class (Sec. 5.1, Eq. 3 discretisation),
  *   3. keeps the N best-scoring classes and places one sample at the centre
  *      of each (Eq. 1 with the class centre as depth),
  *   4. warps each sample towards the view cell (Eq. 4-5) and encodes it,
@@ -72,6 +73,20 @@ typedef enum donerf_select {
                                        fp32 arithmetic; n_bins <= 128          */
 } donerf_select;
 
+typedef enum donerf_depth_input {
+    DONERF_DEPTH_ENCODED = 0,  /* encode(unified origin / d_max, 10) and encode(r, 4):
+                                  90 inputs (layout below)                      */
+    DONERF_DEPTH_POSITIONS = 1 /* Sec. 5.2, App. D: unified origin / d_max, r and
+                                  one position (x_k - c) / d_max per class
+                                  centre, x_k = o + c_k r from the camera origin,
+                                  unencoded: 6 + 3 n_bins inputs in the order
+                                  [origin xyz, r xyz, x_0 xyz, ..., x_{B-1} xyz].
+                                  The first layer's weights are folded at create
+                                  into 9 columns (the positions are affine in the
+                                  ray) and evaluated in fp32 in both precisions;
+                                  its inputs are not rounded to bf16           */
+} donerf_depth_input;
+
 /* Maximum number of samples per ray a handle can be created for. */
 #define DONERF_MAX_SAMPLES 16
 
@@ -88,15 +103,16 @@ typedef struct donerf_cfg {
     float radius;      /* radius > 0 of the unification sphere (Sec. 5.2)      */
     int32_t precision; /* donerf_precision                                     */
     int32_t select;    /* donerf_select                                        */
+    int32_t depth_input; /* donerf_depth_input                                 */
 } donerf_cfg;
 
 /*
- * Number of fp32 values in the weight blob for B depth classes, or 0 if B is
- * not positive.
+ * Number of fp32 values in the weight blob for B depth classes and the given
+ * donerf_depth_input, or 0 if B is not positive or depth_input is unknown.
  *
  * Blob layout (host, fp32): depth network layers 0..7, then shading network
  * layers 0..7; each layer is W[out][in] row-major followed by b[out].
- *   depth  : 90 -> 256, 6 x (256 -> 256), 256 -> B
+ *   depth  : 90 (or 6 + 3 B) -> 256, 6 x (256 -> 256), 256 -> B
  *   shading: 63 -> 256, 6 x (256 -> 256), (256 + 27) -> 4
  * Depth layer 0 reads the encoding of the unified origin divided by d_max
  * (63 values) followed by the encoding of the direction (27 values).  The
@@ -106,7 +122,7 @@ typedef struct donerf_cfg {
  * warped sample (63); shading layer 7 reads the 256 hidden values followed by
  * the direction encoding (27) and outputs (r, g, b, sigma) before activation.
  */
-size_t donerf_weight_count(int32_t n_bins);
+size_t donerf_weight_count(int32_t n_bins, int32_t depth_input);
 
 /*
  * Create a renderer on the current HIP device.
@@ -116,7 +132,8 @@ size_t donerf_weight_count(int32_t n_bins);
  *             on return
  *   out       receives the handle; set to NULL on failure
  * Errors: E_INVALID_ARG (NULL, cfg ranges), E_UNSUPPORTED (n_bins not in the
- * supported set, or above 128 with DONERF_SELECT_CDF), E_SIZE (n_weights != donerf_weight_count(cfg->n_bins)),
+ * supported set, or above 128 with DONERF_SELECT_CDF), E_SIZE (n_weights !=
+ * donerf_weight_count(cfg->n_bins, cfg->depth_input)),
  * E_NONFINITE (NaN/Inf in cfg or weights), E_DEVICE (no device or not
  * gfx950), E_NOMEM, E_HIP.
  */

@@ -30,6 +30,8 @@ BF16 = 1
 SELECT_TOPN = 0
 SELECT_TOPN_SOFTMAX = 1
 SELECT_CDF = 2
+DEPTH_ENCODED = 0
+DEPTH_POSITIONS = 1
 MAX_SAMPLES = 16
 
 # Every function include/donerf.h declares.
@@ -53,7 +55,7 @@ class donerf_cfg(ctypes.Structure):
                 ("n_bins", ctypes.c_int32), ("n_max", ctypes.c_int32),
                 ("fov_x_deg", ctypes.c_float), ("centre", ctypes.c_float * 3),
                 ("radius", ctypes.c_float), ("precision", ctypes.c_int32),
-                ("select", ctypes.c_int32)]
+                ("select", ctypes.c_int32), ("depth_input", ctypes.c_int32)]
 
 
 @dataclass
@@ -67,6 +69,7 @@ class Config:
     radius: float = 1.5
     precision: int = BF16
     select: int = SELECT_TOPN
+    depth_input: int = DEPTH_ENCODED
 
     def to_c(self) -> donerf_cfg:
         c = donerf_cfg()
@@ -76,6 +79,7 @@ class Config:
         c.centre[:] = list(self.centre)
         c.radius = self.radius
         c.precision, c.select = self.precision, self.select
+        c.depth_input = self.depth_input
         return c
 
 
@@ -90,7 +94,7 @@ def lib():
                 f"{LIB_PATH} not built; run `python -m paper_2103_03231_amd.build`")
         L = ctypes.CDLL(LIB_PATH)
         vp, i32, sz, fp = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t, ctypes.POINTER(ctypes.c_float)
-        L.donerf_weight_count.argtypes, L.donerf_weight_count.restype = [i32], sz
+        L.donerf_weight_count.argtypes, L.donerf_weight_count.restype = [i32, i32], sz
         L.donerf_create.argtypes = [ctypes.POINTER(donerf_cfg), fp, sz, ctypes.POINTER(vp)]
         L.donerf_create.restype = ctypes.c_int
         L.donerf_destroy.argtypes, L.donerf_destroy.restype = [vp], None
@@ -118,8 +122,8 @@ def _fptr(a):
     return None if a is None else a.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
 
 
-def donerf_weight_count(n_bins: int) -> int:
-    return int(lib().donerf_weight_count(n_bins))
+def donerf_weight_count(n_bins: int, depth_input: int = DEPTH_ENCODED) -> int:
+    return int(lib().donerf_weight_count(n_bins, depth_input))
 
 
 def donerf_status_str(status: int) -> str:

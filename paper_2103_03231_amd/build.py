@@ -7,6 +7,7 @@ geometry rounds in the written order, and without packed-fp32 instructions.
 """
 from __future__ import annotations
 
+import concurrent.futures
 import os
 import shutil
 import subprocess
@@ -43,12 +44,18 @@ def build(verbose: bool = False, extra: list | None = None) -> str:
     os.makedirs(bdir, exist_ok=True)
     extra = list(extra or [])
     t0 = time.time()
-    objs = []
-    for src in ("kernels.hip", "host.cpp"):
+    srcs = sorted(f for f in os.listdir(CSRC) if f.endswith(".hip")) + ["host.cpp"]
+    cmds, objs = [], []
+    for src in srcs:
         obj = os.path.join(bdir, src + ".o")
         lang = ["-x", "hip"] if src.endswith(".hip") else []
-        _run([hipcc, *COMMON, *extra, *lang, "-c", os.path.join(CSRC, src), "-o", obj], verbose)
+        cmds.append([hipcc, *COMMON, *extra, *lang, "-c", os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)
+    # translation units compile independently; keep a few in flight
+    jobs = max(1, min(len(cmds), int(os.environ.get("MAX_JOBS", "0") or 0) or (os.cpu_count() or 1), 6))
+    with concurrent.futures.ThreadPoolExecutor(jobs) as ex:
+        for f in [ex.submit(_run, c, verbose) for c in cmds]:
+            f.result()
     tmp = LIB + ".tmp"
     _run([hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs], verbose)
     os.replace(tmp, LIB)

@@ -46,6 +46,17 @@ bool finite(float x) { return std::isfinite(x); }
 const int kKinds[16] = {kDFirst, kHiddenL, kHiddenL, kHiddenL, kHiddenL, kHiddenL, kHiddenL, kDHead,
                         kSFirst, kHiddenL, kHiddenL, kHiddenL, kHiddenL, kHiddenL, kHiddenL, kSHead};
 
+// Inputs of the first depth layer in the weight blob.
+int depth_in_cols(int n_bins, int depth_input) {
+    return depth_input == DONERF_DEPTH_POSITIONS ? 6 + 3 * n_bins : kDIn;
+}
+
+// Values of layer l's W in the blob.
+size_t blob_w_count(int l, int n_bins, int depth_input) {
+    const LayerGeom lg = layer_geom(kKinds[l], n_bins);
+    return (size_t)lg.out_rows * (l == 0 ? depth_in_cols(n_bins, depth_input) : lg.in_cols);
+}
+
 bool bins_supported(int B) { return B >= 64 && B <= 256 && B % 64 == 0; }
 
 int validate_cfg(const donerf_cfg* c) {
@@ -68,6 +79,8 @@ int validate_cfg(const donerf_cfg* c) {
     if (c->select != DONERF_SELECT_TOPN && c->select != DONERF_SELECT_TOPN_SOFTMAX &&
         c->select != DONERF_SELECT_CDF)
         return fail(DONERF_E_INVALID_ARG, "unknown select mode");
+    if (c->depth_input != DONERF_DEPTH_ENCODED && c->depth_input != DONERF_DEPTH_POSITIONS)
+        return fail(DONERF_E_INVALID_ARG, "unknown depth_input");
     if (!bins_supported(c->n_bins))
         return fail(DONERF_E_UNSUPPORTED, "n_bins must be 64, 128, 192 or 256");
     if (c->select == DONERF_SELECT_CDF && c->n_bins > 128)
@@ -101,11 +114,52 @@ uint16_t to_bf16(float x) {  // round to nearest even (inputs are finite)
     return (uint16_t)(u >> 16);
 }
 
+float bf16_value(float x) {
+    const uint32_t u = (uint32_t)to_bf16(x) << 16;
+    float f;
+    std::memcpy(&f, &u, 4);
+    return f;
+}
+
+// Folds the first depth layer of the positions input (256 x (6 + 3 B) over
+// [u', r, p_0, ..., p_{B-1}], p_k = u_c + (c_k / d_max) r) into 256 x 9 over
+// [u', r, u_c]: the origin columns stay, the direction columns gain
+// sum_k (c_k / d_max) W_k and the u_c columns are sum_k W_k.  Sums in fp64
+// from the weights as the network uses them (bf16-rounded in bf16 mode),
+// stored as fp32.
+std::vector<float> fold_positions_layer(const float* W, int B, bool bf16, const std::vector<float>& centres,
+                                        float d_max) {
+    const int n_in = 6 + 3 * B;
+    std::vector<float> out((size_t)kHidden * kPIn);
+    for (int u = 0; u < kHidden; ++u) {
+        auto w = [&](int col) -> double {
+            const float v = W[(size_t)u * n_in + col];
+            return bf16 ? (double)bf16_value(v) : (double)v;
+        };
+        double mo[3] = {0.0, 0.0, 0.0}, mr[3] = {0.0, 0.0, 0.0};
+        for (int k = 0; k < B; ++k) {
+            const double s = (double)centres[k] / (double)d_max;
+            for (int j = 0; j < 3; ++j) {
+                const double wk = w(6 + 3 * k + j);
+                mo[j] += wk;
+                mr[j] += s * wk;
+            }
+        }
+        for (int j = 0; j < 3; ++j) {
+            out[(size_t)u * kPIn + j] = (float)w(j);
+            out[(size_t)u * kPIn + 3 + j] = (float)(w(3 + j) + mr[j]);
+            out[(size_t)u * kPIn + 6 + j] = (float)mo[j];
+        }
+    }
+    return out;
+}
+
 // Logical input column of the blob for K step ks, lane group g, element e.
 int in_col(bool bf16, int kind, int ks, int g, int e) {
     const int E = elems(bf16);
     switch (kind) {
         case kDFirst: return d_feature(g, ks * E + e);
+        case kDFirstPos: return p_feature(ks, g, e);
         case kSFirst: return s_feature(g, ks * E + e);
         case kHiddenL:
         case kDHead: return chained_row(bf16, ks, g, e);
@@ -237,7 +291,9 @@ int render_impl(donerf_t* h, const float* poses, int32_t P, int32_t H, int32_t W
         a.n_full = split > 1 ? full : tiles;
         a.split = (int32_t)split;
         a.partial = h->partial;
-        hipError_t e = launch_render(h->bf16, ncap_for(N), place, a, split > 1 ? rem : 0, h->stream);
+        hipError_t e = launch_render(h->bf16, ncap_for(N), place,
+                                     c.depth_input == DONERF_DEPTH_POSITIONS ? kDinPositions : kDinEncoded, a,
+                                     split > 1 ? rem : 0, h->stream);
         if (e != hipSuccess) return hip_fail(e, "render launch");
         if (split > 1) {
             e = launch_combine(h->bf16, a, h->stream);
@@ -255,13 +311,12 @@ int render_impl(donerf_t* h, const float* poses, int32_t P, int32_t H, int32_t W
 
 extern "C" {
 
-size_t donerf_weight_count(int32_t n_bins) {
+size_t donerf_weight_count(int32_t n_bins, int32_t depth_input) {
     if (n_bins < 1) return 0;
+    if (depth_input != DONERF_DEPTH_ENCODED && depth_input != DONERF_DEPTH_POSITIONS) return 0;
     size_t n = 0;
-    for (int l = 0; l < 16; ++l) {
-        const LayerGeom lg = layer_geom(kKinds[l], n_bins);
-        n += (size_t)lg.out_rows * lg.in_cols + lg.out_rows;
-    }
+    for (int l = 0; l < 16; ++l)
+        n += blob_w_count(l, n_bins, depth_input) + (size_t)layer_geom(kKinds[l], n_bins).out_rows;
     return n;
 }
 
@@ -272,7 +327,7 @@ int donerf_create(const donerf_cfg* cfg, const float* weights, size_t n_weights,
     int rc = validate_cfg(cfg);
     if (rc) return rc;
     if (!weights) return fail(DONERF_E_INVALID_ARG, "weights is NULL");
-    const size_t want = donerf_weight_count(cfg->n_bins);
+    const size_t want = donerf_weight_count(cfg->n_bins, cfg->depth_input);
     if (n_weights != want)
         return fail(DONERF_E_SIZE, "weight count " + std::to_string(n_weights) + " != " + std::to_string(want));
     for (size_t k = 0; k < n_weights; ++k)
@@ -283,16 +338,24 @@ int donerf_create(const donerf_cfg* cfg, const float* weights, size_t n_weights,
 
     const bool bf16 = cfg->precision == DONERF_BF16;
     const int B = cfg->n_bins;
+    const bool positions = cfg->depth_input == DONERF_DEPTH_POSITIONS;
+    std::vector<float> bounds, centres, widths;
+    make_bins(*cfg, bounds, centres, widths);
     std::vector<uint8_t> frags;
     std::vector<float> bias;
     int n_d_chunks = 0, n_s_chunks = 0;
     size_t off = 0;
     for (int l = 0; l < 16; ++l) {
-        const int kind = kKinds[l];
+        const int kind = (l == 0 && positions) ? kDFirstPos : kKinds[l];
         const LayerGeom lg = layer_geom(kind, B);
-        pack_layer(bf16, kind, B, weights + off, frags);
+        if (kind == kDFirstPos) {
+            const std::vector<float> folded = fold_positions_layer(weights + off, B, bf16, centres, cfg->far_dist);
+            pack_layer(false, kind, B, folded.data(), frags);
+        } else {
+            pack_layer(bf16, kind, B, weights + off, frags);
+        }
         (l < 8 ? n_d_chunks : n_s_chunks) += layer_chunks(bf16, kind, B);
-        off += (size_t)lg.out_rows * lg.in_cols;
+        off += blob_w_count(l, B, cfg->depth_input);
         const size_t b0 = bias.size();
         bias.resize(b0 + bias_len(kind, B), 0.0f);
         std::memcpy(bias.data() + b0, weights + off, sizeof(float) * lg.out_rows);
@@ -308,7 +371,9 @@ int donerf_create(const donerf_cfg* cfg, const float* weights, size_t n_weights,
     h->n_d_chunks = n_d_chunks;
     h->n_s_chunks = n_s_chunks;
     h->bias_len = (int)bias.size();
-    make_bins(*cfg, h->h_bounds, h->h_centres, h->h_widths);
+    h->h_bounds = bounds;
+    h->h_centres = centres;
+    h->h_widths = widths;
     std::vector<float> bins(2 * B);
     std::memcpy(bins.data(), h->h_centres.data(), sizeof(float) * B);
     std::memcpy(bins.data() + B, h->h_widths.data(), sizeof(float) * B);

@@ -62,9 +62,14 @@ constexpr int kBf16Occ = DONERF_BF16_OCC;
 inline int rays_per_block(bool bf16) { return bf16 ? kBf16NW * 32 * kBf16CB : 4 * 32; }
 
 // Launches a.n_full whole tiles plus n_split_tiles tiles split a.split ways.
-// place: 0 top-N, 1 inverse CDF.
-hipError_t launch_render(bool bf16, int ncap, int place, const RenderArgs& a, uint32_t n_split_tiles,
+// place: layout.h Placement; din: layout.h DepthInput.
+hipError_t launch_render(bool bf16, int ncap, int place, int din, const RenderArgs& a, uint32_t n_split_tiles,
                          hipStream_t stream);
+// The variants of one precision and placement (render_*.hip).
+hipError_t launch_render_bf16_topn(int ncap, int din, const RenderArgs& a, dim3 grid, hipStream_t stream);
+hipError_t launch_render_bf16_cdf(int ncap, int din, const RenderArgs& a, dim3 grid, hipStream_t stream);
+hipError_t launch_render_fp32_topn(int ncap, int din, const RenderArgs& a, dim3 grid, hipStream_t stream);
+hipError_t launch_render_fp32_cdf(int ncap, int din, const RenderArgs& a, dim3 grid, hipStream_t stream);
 // Composites the split parts of rays [n_full * rays_per_block, total_rays)
 // into out_rgb / out_depth.
 hipError_t launch_combine(bool bf16, const RenderArgs& a, hipStream_t stream);

@@ -109,8 +109,25 @@ DN_HD constexpr int skip_feature(int g, int s) {
 constexpr int kSkipSlots = 16;
 constexpr int kSkipKPad = 32;
 
-// Layer roles in the streamed weight sequence.
-enum LayerKind { kDFirst = 0, kHiddenL = 1, kDHead = 2, kSFirst = 3, kSHead = 4 };
+// Depth network input of the paper (Sec. 5.2): unified origin, direction and
+// one position per class centre, unencoded, 6 + 3 B values.  Position k is
+// ((o - c) + c_k r) / d_max, so the layer's weights fold (host.cpp) into a
+// 9-column layer over [u' (3), r (3), u_c (3)], u' = (o' - c) / d_max,
+// u_c = (o - c) / d_max, run as fp32 fragments (K padded to 16).  K slot
+// 8 ks + 2 e + g of the fp32 layout holds folded column K (< 9) or zero.
+constexpr int kPIn = 9;
+constexpr int kPKPad = 16;
+DN_HD constexpr int p_feature(int ks, int g, int e) {
+    return 8 * ks + 2 * e + g < kPIn ? 8 * ks + 2 * e + g : -1;
+}
+
+// Sample placement and depth-network input of a render variant.
+enum Placement { kPlaceTopN = 0, kPlaceCdf = 1 };
+enum DepthInput { kDinEncoded = 0, kDinPositions = 1 };
+
+// Layer roles in the streamed weight sequence.  kDFirstPos is the folded
+// first depth layer of the positions input.
+enum LayerKind { kDFirst = 0, kHiddenL = 1, kDHead = 2, kSFirst = 3, kSHead = 4, kDFirstPos = 5 };
 
 struct LayerGeom {
     int out_rows;   // logical output units
@@ -122,15 +139,20 @@ struct LayerGeom {
 
 DN_HD constexpr LayerGeom layer_geom(int kind, int n_bins) {
     return kind == kDFirst  ? LayerGeom{kHidden, kDIn, kDKPad, 8, kRbPerPass}
+         : kind == kDFirstPos ? LayerGeom{kHidden, kPIn, kPKPad, 8, kRbPerPass}
          : kind == kHiddenL ? LayerGeom{kHidden, kHidden, kHidden, 8, kRbPerPass}
          : kind == kDHead   ? LayerGeom{n_bins, kHidden, kHidden, n_bins / 32, kRbPerPass}
          : kind == kSFirst  ? LayerGeom{kHidden, kSIn, kSKPad, 8, kRbPerPass}
          :                    LayerGeom{kSOut, kHidden + kSkip, kHidden + kSkipKPad, 1, 1};
 }
 
+// Whether a layer's fragments are bf16 in a network of the given precision
+// (the folded positions layer is fp32 in both).
+DN_HD constexpr bool frag_bf16(bool bf16, int kind) { return kind == kDFirstPos ? false : bf16; }
+
 // Fragments a layer streams (before padding to whole chunks).
 DN_HD constexpr int layer_frags(bool bf16, int kind, int n_bins) {
-    return layer_geom(kind, n_bins).rb * ksteps(bf16, layer_geom(kind, n_bins).kpad);
+    return layer_geom(kind, n_bins).rb * ksteps(frag_bf16(bf16, kind), layer_geom(kind, n_bins).kpad);
 }
 DN_HD constexpr int layer_chunks(bool bf16, int kind, int n_bins) {
     return (layer_frags(bf16, kind, n_bins) + kChunkFrags - 1) / kChunkFrags;

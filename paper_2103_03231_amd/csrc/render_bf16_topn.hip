@@ -1,0 +1,12 @@
+// render_bf16_topn.hip - render kernels with bf16 networks (fp32 accumulation) and top-N placement,
+// both depth-network inputs.  One translation unit per precision and
+// placement so that the variants compile in parallel.
+#include "render_kernel.h"
+
+namespace donerf {
+
+hipError_t launch_render_bf16_topn(int ncap, int din, const RenderArgs& a, dim3 grid, hipStream_t stream) {
+    return launch_placement<true, kBf16CB, kBf16NW, kBf16Occ, kPlaceTopN>(ncap, din, a, grid, stream);
+}
+
+}  // namespace donerf

@@ -1,0 +1,896 @@
+// render_kernel.h - the fused DONeRF per-ray kernel for gfx950 (MI355X).
+//
+// One workgroup renders a tile of rays: ray generation and unification
+// (Sec. 5.2), the depth-network input (encoded, Eq. 2, or the unencoded
+// positions of Sec. 5.2), the depth-oracle network (App. D) on MFMA, the
+// choice of samples (top-N classes in registers, or the inverse CDF of
+// Sec. 5.1), the space warp (Eq. 4-5) and encoding, the shading network on
+// MFMA with the encoded direction skipped into its last layer (App. D), and
+// front-to-back compositing over black.  The only HBM traffic is the streamed
+// weights (L2-resident after first touch) and the output pixels.
+//
+// Work split (bf16): 8 waves per workgroup, two per SIMD, one workgroup per
+// CU.  Each wave owns 32 * CB rays (the MFMA columns); the workgroup shares
+// one stream of weight fragments through a ring of kRing LDS chunks, so each
+// weight byte read from L2 feeds every wave.  Activations never leave the
+// registers: accumulators of layer l become, after bias, ReLU and rounding,
+// the B operand of layer l+1 (layout.h explains the K permutation that makes
+// this possible).
+//
+// Included by the render_*.hip translation units, each of which instantiates
+// the variants of one precision and placement; everything here has internal
+// linkage.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <utility>
+
+#include "internal.h"
+
+namespace donerf {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// ------------------------------------------------------------------ compile-time loops
+
+template <class F, int... I>
+__device__ __forceinline__ void sfor_impl(F& f, std::integer_sequence<int, I...>) {
+    (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void sfor(F&& f) {
+    sfor_impl(f, std::make_integer_sequence<int, N>{});
+}
+#define CV(x) decltype(x)::value
+
+// ------------------------------------------------------------------ precision traits
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    f32x2 v = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
+
+template <bool BF16>
+struct Prec;
+
+template <>
+struct Prec<true> {
+    static constexpr int E = 8;      // K elements per lane per fragment
+    static constexpr int KSPB = 2;   // K steps produced per 32-row block
+    __device__ static __forceinline__ f32x16 mma(u32x4 a, u32x4 b, f32x16 c) {
+        return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                       __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+    }
+    __device__ static __forceinline__ u32x4 pack(const float* f) {
+        return u32x4{pack_bf16x2(f[0], f[1]), pack_bf16x2(f[2], f[3]),
+                     pack_bf16x2(f[4], f[5]), pack_bf16x2(f[6], f[7])};
+    }
+};
+
+template <>
+struct Prec<false> {
+    static constexpr int E = 4;
+    static constexpr int KSPB = 4;
+    __device__ static __forceinline__ f32x16 mma(u32x4 a, u32x4 b, f32x16 c) {
+        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
+        return c;
+    }
+    __device__ static __forceinline__ u32x4 pack(const float* f) {
+        return u32x4{__float_as_uint(f[0]), __float_as_uint(f[1]), __float_as_uint(f[2]),
+                     __float_as_uint(f[3])};
+    }
+};
+
+// ------------------------------------------------------------------ LDS weight stream
+
+__device__ __forceinline__ void lds_barrier() {
+    // Orders LDS traffic only; outstanding global prefetches stay in flight.
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+constexpr int kChunkVec = kChunkBytes / 16;  // u32x4 per chunk
+#ifndef DONERF_FRAG_AHEAD
+#define DONERF_FRAG_AHEAD 3
+#endif
+constexpr int kFragAhead = DONERF_FRAG_AHEAD;  // LDS fragment reads in flight
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
+template <int VM>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(VM >= 0 && VM < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// The workgroup consumes one logical sequence of chunks: every depth-network
+// chunk, then the shading-network chunks once per sample.  Chunks travel
+// from L2 straight into LDS (global_load_lds, 16 bytes per lane), kRing - 1
+// chunks ahead of use, in a ring of kRing slots.  Each wave copies
+// kChunkFrags / NW fragments of every chunk; advancing to chunk c waits for
+// the wave's own copies of c (later chunks stay in flight) and then
+// barriers, which both publishes c and retires every reader of chunk c-1,
+// whose slot the copy of chunk c + kRing - 1 then reuses.  The copy count per
+// step is constant (the stream index is clamped past its end) so the counter
+// arithmetic holds at the tail.
+template <int NW>
+struct WeightStream {
+    static constexpr int FPW = kChunkFrags / NW;  // fragments each wave copies per chunk
+    static constexpr int AHEAD = kRing - 1;
+    static_assert(kChunkFrags % NW == 0, "chunk split");
+    const u32x4* dsrc;
+    const u32x4* ssrc;
+    u32x4* ring;
+    int nd, ns, total;
+    int c;       // chunk being consumed
+    int slot;    // its LDS slot
+    int lane, wave;
+    int src_k;   // stream index of the next chunk to copy (clamped to total - 1)
+    int src_s;   // its position in the shading-network chunks (mod ns)
+
+    // Branch-free (selects only), so chunk changes do not split the
+    // scheduling region of the MFMA stream around them.
+    __device__ __forceinline__ void issue(int dst_slot) {
+        const bool in_d = src_k < nd;
+        const u32x4* base = in_d ? dsrc : ssrc;
+        const int off = in_d ? src_k : src_s;
+        const u32x4* sp = base + (size_t)off * kChunkVec + wave * FPW * 64 + lane;
+        u32x4* dp = ring + dst_slot * kChunkVec + wave * FPW * 64;
+#pragma unroll
+        for (int i = 0; i < FPW; ++i)
+            __builtin_amdgcn_global_load_lds(sp + i * 64, dp + i * 64, 16, 0, 0);
+        const int nk = src_k + 1;
+        const bool adv = nk < total;
+        src_s = (adv && nk > nd) ? (src_s + 1 == ns ? 0 : src_s + 1) : src_s;
+        src_k = adv ? nk : src_k;
+    }
+    __device__ __forceinline__ void start() {
+        c = -1;
+        slot = kRing - 1;
+        src_k = 0;
+        src_s = 0;
+#pragma unroll
+        for (int k = 0; k < AHEAD; ++k) issue(k);
+    }
+    __device__ __forceinline__ void next() {
+        ++c;
+        slot = slot == kRing - 1 ? 0 : slot + 1;
+        wait_vmcnt<FPW * (AHEAD - 1)>();
+        lds_barrier();
+        // the slot of chunk c - 1, i.e. the one before c's in ring order
+        issue(slot == 0 ? kRing - 1 : slot - 1);
+    }
+    __device__ __forceinline__ void finish() { wait_vmcnt<0>(); }
+    __device__ __forceinline__ u32x4 frag(int i) const { return ring[slot * kChunkVec + i * 64 + lane]; }
+};
+
+// ------------------------------------------------------------------ MFMA layers
+
+// Accumulator initialised with the bias of 32-row block r: lane group g holds
+// rows 8q + 4g + j (q, j = 0..3) in register 4q + j.
+__device__ __forceinline__ f32x16 bias_frag(const float* bias, int g) {
+    f32x16 b;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(bias + 8 * q + 4 * g);
+        b[4 * q + 0] = v[0];
+        b[4 * q + 1] = v[1];
+        b[4 * q + 2] = v[2];
+        b[4 * q + 3] = v[3];
+    }
+    return b;
+}
+
+// One accumulator pass: RBP output row blocks x CB column blocks over KS K
+// steps.  BASE is the index of the pass's first fragment within its layer;
+// layers start on chunk boundaries, so chunk changes are known statically.
+template <bool BF16, int CB, int KS, int RBP, int BASE, class WS, class GetB, class Epi>
+__device__ __forceinline__ void run_pass(WS& st, int g, const float* bias, GetB& getB, Epi&& epi) {
+    using P = Prec<BF16>;
+    constexpr int NF = KS * RBP;   // fragments of the pass, in (K step, row block) order
+    constexpr int D = kFragAhead;  // LDS reads issued this many fragments ahead
+    f32x16 acc[RBP][CB];
+    sfor<RBP>([&](auto R) {
+        const f32x16 b = bias_frag(bias + 32 * CV(R), g);
+        sfor<CB>([&](auto C) { acc[CV(R)][CV(C)] = b; });
+    });
+    u32x4 a[NF];
+    // Software pipeline: step s reads fragment s and multiplies fragment
+    // s - D.  The scheduling barriers keep LDS reads and MFMAs in this order
+    // (bounding the registers held by fragments in flight) while VALU and
+    // SALU work may move across them.
+    sfor<NF + D>([&](auto S) {
+        constexpr int s = CV(S);
+        if constexpr (s < NF) {
+            constexpr int idx = BASE + s;
+            if constexpr (idx % kChunkFrags == 0) st.next();
+            a[s] = st.frag(idx % kChunkFrags);
+        }
+        if constexpr (s >= D) {
+            constexpr int f = s - D;
+            constexpr int k = f / RBP, r = f % RBP;
+            sfor<CB>([&](auto C) {
+                acc[r][CV(C)] = P::mma(a[f], getB(std::integral_constant<int, k>{}, C), acc[r][CV(C)]);
+            });
+        }
+        __builtin_amdgcn_sched_barrier(0x6);
+    });
+    sfor<RBP>([&](auto R) { sfor<CB>([&](auto C) { epi(R, C, acc[CV(R)][CV(C)]); }); });
+}
+
+// ReLU, round, and place a 32-row accumulator block as K steps
+// [ks0, ks0 + KSPB) of the next layer's B operand.  bf16: round to nearest
+// even, then ReLU on the packed pair as a signed 16-bit max with 0 (rounding
+// preserves the sign, so this equals rounding the ReLU).
+template <bool BF16, int NK, int CB>
+__device__ __forceinline__ void emit_relu(const f32x16& acc, u32x4 (&out)[NK][CB], int ks0, int cb) {
+    using P = Prec<BF16>;
+    if constexpr (BF16) {
+        typedef short i16x2 __attribute__((ext_vector_type(2)));
+#pragma unroll
+        for (int h = 0; h < P::KSPB; ++h) {
+            u32x4 o;
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+                const i16x2 v = __builtin_bit_cast(i16x2, pack_bf16x2(acc[8 * h + 2 * w], acc[8 * h + 2 * w + 1]));
+                o[w] = __builtin_bit_cast(uint32_t, __builtin_elementwise_max(v, i16x2{0, 0}));
+            }
+            out[ks0 + h][cb] = o;
+        }
+    } else {
+        float v[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) v[i] = fmaxf(acc[i], 0.0f);
+#pragma unroll
+        for (int h = 0; h < P::KSPB; ++h) out[ks0 + h][cb] = P::pack(v + h * P::E);
+    }
+}
+
+// Fully connected ReLU layer with 256 outputs (8 row blocks) as one software
+// pipeline over its KS * 8 fragments: passes of kRbPerPass row blocks use
+// alternating accumulator sets, so the bias/ReLU/rounding of pass p can
+// overlap the MFMAs of pass p + 1, and LDS reads run kFragAhead fragments
+// ahead across pass and chunk boundaries.  BF16 is the precision of the
+// output activations; MMA_BF16 that of the layer's own fragments and input
+// (an fp32 layer may feed a bf16 network).
+template <bool BF16, int CB, int KS, bool MMA_BF16 = BF16, class WS, class GetB>
+__device__ __forceinline__ void hidden_layer(WS& st, int g, const float* bias, GetB&& getB,
+                                             u32x4 (&out)[8 * Prec<BF16>::KSPB][CB]) {
+    using P = Prec<BF16>;
+    using M = Prec<MMA_BF16>;
+    constexpr int RBP = kRbPerPass;
+    constexpr int PF = KS * RBP;       // fragments per pass
+    constexpr int NF = 8 * KS;         // fragments of the layer
+    constexpr int D = kFragAhead;
+    f32x16 acc[2][RBP][CB];
+    u32x4 a[D + 1];
+    sfor<NF + D>([&](auto S) {
+        constexpr int s = CV(S);
+        if constexpr (s < NF) {
+            if constexpr (s % kChunkFrags == 0) st.next();
+            a[s % (D + 1)] = st.frag(s % kChunkFrags);
+        }
+        if constexpr (s >= D) {
+            constexpr int f = s - D;
+            constexpr int p = f / PF, w = f % PF, k = w / RBP, r = w % RBP;
+            if constexpr (w == 0) {
+                sfor<RBP>([&](auto R) {
+                    const f32x16 b = bias_frag(bias + 32 * (RBP * p + CV(R)), g);
+                    sfor<CB>([&](auto C) { acc[p & 1][CV(R)][CV(C)] = b; });
+                });
+            }
+            sfor<CB>([&](auto C) {
+                acc[p & 1][r][CV(C)] = M::mma(a[f % (D + 1)], getB(std::integral_constant<int, k>{}, C),
+                                              acc[p & 1][r][CV(C)]);
+            });
+            if constexpr (w == PF - 1) {
+                sfor<RBP>([&](auto R) {
+                    sfor<CB>([&](auto C) {
+                        emit_relu<BF16>(acc[p & 1][CV(R)][CV(C)], out, (p * RBP + CV(R)) * P::KSPB, CV(C));
+                    });
+                });
+            }
+        }
+        __builtin_amdgcn_sched_barrier(0x6);
+    });
+}
+
+// ------------------------------------------------------------------ selection
+
+// Best-first list of (score, class) under the order: higher score first,
+// lower class index first among equal scores.
+template <int NCAP>
+struct TopList {
+    float v[NCAP];
+    int i[NCAP];
+    __device__ __forceinline__ void init() {
+#pragma unroll
+        for (int k = 0; k < NCAP; ++k) {
+            v[k] = -INFINITY;
+            i[k] = 0x7fff;
+        }
+    }
+    __device__ __forceinline__ void place(const bool (&c)[NCAP], float x, int ix) {
+        // c is monotone (c[k] implies c[k+1]); shift the tail down by one.
+#pragma unroll
+        for (int k = NCAP - 1; k > 0; --k) {
+            v[k] = c[k - 1] ? v[k - 1] : (c[k] ? x : v[k]);
+            i[k] = c[k - 1] ? i[k - 1] : (c[k] ? ix : i[k]);
+        }
+        v[0] = c[0] ? x : v[0];
+        i[0] = c[0] ? ix : i[0];
+    }
+    // Insert a class whose index exceeds every index already held.
+    __device__ __forceinline__ void push_ascending(float x, int ix) {
+        bool c[NCAP];
+#pragma unroll
+        for (int k = 0; k < NCAP; ++k) c[k] = x > v[k];
+        place(c, x, ix);
+    }
+    // Insert any class.
+    __device__ __forceinline__ void push(float x, int ix) {
+        bool c[NCAP];
+#pragma unroll
+        for (int k = 0; k < NCAP; ++k) c[k] = x > v[k] || (x == v[k] && ix < i[k]);
+        place(c, x, ix);
+    }
+    // Merge with the list of lane l ^ 32 (the other half of the same ray's
+    // classes); both lanes end with the same list.
+    __device__ __forceinline__ void merge_partner() {
+        float pv[NCAP];
+        int pi[NCAP];
+#pragma unroll
+        for (int k = 0; k < NCAP; ++k) {
+            pv[k] = __shfl_xor(v[k], 32);
+            pi[k] = __shfl_xor(i[k], 32);
+        }
+#pragma unroll
+        for (int k = 0; k < NCAP; ++k) push(pv[k], pi[k]);
+    }
+    // The first N classes in ascending index order in s[0..N), padding after.
+    __device__ __forceinline__ void ascending(int N, int (&s)[NCAP]) const {
+#pragma unroll
+        for (int k = 0; k < NCAP; ++k) s[k] = k < N ? i[k] : 0x7fff;
+#pragma unroll
+        for (int round = 0; round < NCAP; ++round) {
+#pragma unroll
+            for (int k = round & 1; k + 1 < NCAP; k += 2) {
+                const int a = s[k], b = s[k + 1];
+                s[k] = min(a, b);
+                s[k + 1] = max(a, b);
+            }
+        }
+    }
+};
+
+template <int NCAP>
+__device__ __forceinline__ int pick(const int (&s)[NCAP], int k) {
+    int r = s[0];
+#pragma unroll
+    for (int q = 1; q < NCAP; ++q) r = k == q ? s[q] : r;
+    return r;
+}
+
+__device__ __forceinline__ float pick_f(const float* v, int n, int k) {
+    float r = v[0];
+    for (int q = 1; q < n; ++q) r = k == q ? v[q] : r;
+    return r;
+}
+
+// ------------------------------------------------------------------ inverse-CDF placement
+
+// Sample placement of Sec. 5.1 (Fig. 7): the class values sigmoid(score)
+// form a piecewise-constant PDF over the classes (uniform in the coordinate
+// of Eq. 3); the CDF is inverted at u_i = (i + 0.5) / N, and each sample's
+// width is the depth extent of its probability slice [i/N, (i+1)/N].
+//
+// v[P][R][i] holds this lane's class values for class 32 (P * RBP + R) +
+// 8 (i/4) + 4 g + i%4, i.e. lane-local blocks of four consecutive classes;
+// global block b = 2 * local + g alternates between the lane pair.  Both
+// lanes build the same prefix over the blocks (the partner's block sums
+// arrive by a lane swap), locate each target's block by counting the blocks
+// that end at or below it, and take the block's four values from the lane
+// that owns it.  Everything is fp32.
+template <int NPM, int NCAP>
+__device__ __forceinline__ void cdf_place(const float (&v)[NPM][kRbPerPass][16], int g, int N, int B,
+                                          float near, float far, float log2_span1, float (&ts)[NCAP],
+                                          float (&ds)[NCAP], int (&cls)[NCAP]) {
+    constexpr int NLB = NPM * kRbPerPass * 4;  // lane-local blocks
+    constexpr int NB = 2 * NLB;                // blocks in class order
+    float bs[NLB], pbs[NLB];
+#pragma unroll
+    for (int P = 0; P < NPM; ++P)
+#pragma unroll
+        for (int R = 0; R < kRbPerPass; ++R)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                bs[(P * kRbPerPass + R) * 4 + q] =
+                    ((v[P][R][4 * q] + v[P][R][4 * q + 1]) + v[P][R][4 * q + 2]) + v[P][R][4 * q + 3];
+#pragma unroll
+    for (int lb = 0; lb < NLB; ++lb) pbs[lb] = __shfl_xor(bs[lb], 32);
+    float pre[NB + 1];
+    pre[0] = 0.0f;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) pre[b + 1] = pre[b] + (((b & 1) == g) ? bs[b >> 1] : pbs[b >> 1]);
+    const float total = pre[NB];
+
+    // coordinate s in [0, 1] of the target fraction u; k: its class
+    auto inverse = [&](float u, int& k) {
+        const float m = u * total;
+        int b = 0;
+#pragma unroll
+        for (int bb = 0; bb < NB; ++bb) b += pre[bb + 1] <= m ? 1 : 0;
+        b = min(b, NB - 1);
+        const int lb = b >> 1;
+        float w[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            float r = 0.0f;
+#pragma unroll
+            for (int P = 0; P < NPM; ++P)
+#pragma unroll
+                for (int R = 0; R < kRbPerPass; ++R)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        r = lb == (P * kRbPerPass + R) * 4 + q ? v[P][R][4 * q + j] : r;
+            w[j] = r;
+        }
+        const bool own = (b & 1) == g;
+        float a4[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const float pw = __shfl_xor(w[j], 32);
+            a4[j] = own ? w[j] : pw;
+        }
+        float lo = pre[0];
+#pragma unroll
+        for (int bb = 1; bb < NB; ++bb) lo = b == bb ? pre[bb] : lo;
+        const float c1 = lo + a4[0], c2 = c1 + a4[1], c3 = c2 + a4[2];
+        const int j = (m >= c1 ? 1 : 0) + (m >= c2 ? 1 : 0) + (m >= c3 ? 1 : 0);
+        const float base = j == 0 ? lo : j == 1 ? c1 : j == 2 ? c2 : c3;
+        const float aj = j == 0 ? a4[0] : j == 1 ? a4[1] : j == 2 ? a4[2] : a4[3];
+        const float frac = aj > 0.0f ? fminf(fmaxf((m - base) / aj, 0.0f), 1.0f) : 0.0f;
+        k = 4 * b + j;
+        return ((float)k + frac) / (float)B;
+    };
+    auto to_depth = [&](float s) { return near + exp2f(s * log2_span1) - 1.0f; };  // inverse of Eq. 3
+    float edge[NCAP + 1];
+    edge[0] = near;
+#pragma unroll
+    for (int i = 0; i < NCAP; ++i) {
+        if (i < N) {
+            int k;
+            ts[i] = to_depth(inverse(((float)i + 0.5f) / (float)N, k));
+            cls[i] = k;
+            int kk;
+            edge[i + 1] = i + 1 < N ? to_depth(inverse((float)(i + 1) / (float)N, kk)) : far;
+        } else {
+            ts[i] = far;
+            cls[i] = B - 1;
+            edge[i + 1] = far;
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < NCAP; ++i) ds[i] = edge[i + 1] - edge[i];
+}
+
+// ------------------------------------------------------------------ geometry (fp32, fixed order)
+// Built with -ffp-contract=off: every operation below rounds to fp32 in the
+// written order.  Divides and sqrtf are correctly rounded (hipcc's default
+// expansions); __fsqrt_rn is not used because it lowers to the bare hardware
+// square root, which can be one ulp off, and the encoding multiplies an ulp
+// of the ray geometry by up to 2^9 pi.
+
+struct Ray {
+    float o[3], r[3];
+};
+
+__device__ __forceinline__ Ray camera_ray(const RenderArgs& a, uint32_t ray) {
+    const uint32_t hw = (uint32_t)a.H * (uint32_t)a.W;
+    const uint32_t p = ray / hw;
+    const uint32_t pix = ray - p * hw;
+    const uint32_t j = pix / (uint32_t)a.W;
+    const uint32_t i = pix - j * (uint32_t)a.W;
+    const float u = (((float)i + 0.5f) - a.half_w) / a.focal;
+    const float v = -((((float)j + 0.5f) - a.half_h) / a.focal);
+    const float* M = a.poses[p];
+    float d[3];
+#pragma unroll
+    for (int k = 0; k < 3; ++k) d[k] = (M[4 * k + 0] * u + M[4 * k + 1] * v) + M[4 * k + 2] * -1.0f;
+    const float n = sqrtf((d[0] * d[0] + d[1] * d[1]) + d[2] * d[2]);
+    Ray out;
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+        out.r[k] = d[k] / n;
+        out.o[k] = M[4 * k + 3];
+    }
+    return out;
+}
+
+// Sec. 5.2: the forward intersection with the sphere |x - c| = R, t >= 0.
+__device__ __forceinline__ void unify(const RenderArgs& a, const Ray& ray, float (&ou)[3]) {
+    const float q0 = ray.o[0] - a.cx, q1 = ray.o[1] - a.cy, q2 = ray.o[2] - a.cz;
+    const float b = (ray.r[0] * q0 + ray.r[1] * q1) + ray.r[2] * q2;
+    const float k = ((q0 * q0 + q1 * q1) + q2 * q2) - a.radius * a.radius;
+    const float disc = fmaxf(b * b - k, 0.0f);
+    const float t = fmaxf(-b + sqrtf(disc), 0.0f);
+#pragma unroll
+    for (int c = 0; c < 3; ++c) ou[c] = ray.o[c] + t * ray.r[c];
+}
+
+// Eq. 4-5: w = p / sqrt(|p| d_max), p = x - c, w = 0 at p = 0.
+__device__ __forceinline__ void warp(const RenderArgs& a, const float (&x)[3], float (&w)[3]) {
+    const float p0 = x[0] - a.cx, p1 = x[1] - a.cy, p2 = x[2] - a.cz;
+    const float n = sqrtf((p0 * p0 + p1 * p1) + p2 * p2);
+    const float s = sqrtf(n * a.dmax);
+    const bool z = n == 0.0f;
+    w[0] = z ? 0.0f : p0 / s;
+    w[1] = z ? 0.0f : p1 / s;
+    w[2] = z ? 0.0f : p2 / s;
+}
+
+// Encoding slots: T frequency pairs 2t + g (t < T) of v, written as
+// [sin x, sin y, sin z, cos x, cos y, cos z] per frequency.  The scale 2^k is
+// exact in fp32 and sincospi avoids multiplying by a rounded pi.  With EXACT
+// false (bf16 networks) only frequencies 2t + g with t % 3 == 0 are evaluated
+// directly; the others follow by two double-angle steps each,
+// sin 2a = 2 sin a cos a and cos 2a = (cos a - sin a)(cos a + sin a), whose
+// error (at most four steps from a direct value, about 16 fp32 ulp) stays far
+// below the bf16 rounding the features then undergo.
+#ifndef DONERF_PE_EXACT
+#define DONERF_PE_EXACT 0
+#endif
+template <int T, bool EXACT>
+__device__ __forceinline__ void fourier(const float (&v)[3], int g, float* f) {
+    const float gs = g ? 2.0f : 1.0f;
+#pragma unroll
+    for (int c = 0; c < 3; ++c) {
+        float s = 0.0f, co = 1.0f;
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+            if (EXACT || DONERF_PE_EXACT || t % 3 == 0) {
+                const float sc = (float)(1u << (2 * t)) * gs;
+                sincospif(v[c] * sc, &s, &co);
+            } else {
+#pragma unroll
+                for (int d = 0; d < 2; ++d) {
+                    const float s2 = (s + s) * co;
+                    co = (co - s) * (co + s);
+                    s = s2;
+                }
+            }
+            f[6 * t + c] = s;
+            f[6 * t + 3 + c] = co;
+        }
+    }
+}
+
+// ------------------------------------------------------------------ fused kernel
+
+constexpr int kBiasMax = 7 * 256 + 256 + 7 * 256 + 32;
+
+// BF16: network precision.  CB: 32-ray column blocks per wave.  NW: waves per
+// workgroup.  OCC: waves per SIMD the register budget is sized for (with
+// OCC * 4 > NW several workgroups share a CU).  NCAP: capacity of the top-N
+// list (top-N) or of the sample arrays (CDF).  PLACE: sample placement.
+// DIN: depth-network input (layout.h DepthInput).
+template <bool BF16, int CB, int NW, int OCC, int NCAP, int PLACE, int DIN>
+__global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(OCC, OCC)))
+render_kernel(const RenderArgs a) {
+    using P = Prec<BF16>;
+    constexpr int E = P::E;
+    // first depth layer: K steps of the encoded input (network precision) or
+    // of the folded positions input (always fp32 fragments, 8 K per step)
+    constexpr int KS_D0 = DIN == kDinEncoded ? kDKPad / (2 * E) : kPKPad / (2 * Prec<false>::E);
+    constexpr int KS_H = kHidden / (2 * E);    // 16 | 32
+    constexpr int KS_S0 = kSKPad / (2 * E);    // 4 | 8
+    constexpr int KS_SK = kSkipKPad / (2 * E); // 2 | 4
+
+    __shared__ u32x4 ring[kRing * kChunkVec];
+    __shared__ float bias_s[kBiasMax];
+    __shared__ float bins_s[2 * 256];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int g = lane >> 5;
+    const int col = lane & 31;
+
+    for (int k = tid; k < a.bias_len; k += 64 * NW) bias_s[k] = a.bias[k];
+    for (int k = tid; k < 2 * a.B; k += 64 * NW) bins_s[k] = a.bins[k];
+
+    WeightStream<NW> st;
+    st.dsrc = reinterpret_cast<const u32x4*>(a.d_frags);
+    st.ssrc = reinterpret_cast<const u32x4*>(a.s_frags);
+    st.ring = ring;
+    st.nd = a.n_d_chunks;
+    st.ns = a.n_s_chunks;
+    // this workgroup's tile and its share of the samples
+    const bool split_part = blockIdx.x >= a.n_full;
+    const uint32_t cpart = blockIdx.x - a.n_full;
+    const int nsplit = split_part ? a.split : 1;
+    const int part = split_part ? (int)(cpart % (uint32_t)a.split) : 0;
+    const uint32_t tile_local = split_part ? cpart / (uint32_t)a.split : 0;
+    const uint32_t tile = split_part ? a.n_full + tile_local : blockIdx.x;
+    const int k_begin = part * a.N / nsplit;
+    const int k_end = (part + 1) * a.N / nsplit;
+    st.total = a.n_d_chunks + (k_end - k_begin) * a.n_s_chunks;
+    st.lane = lane;
+    st.wave = wave;
+    st.start();
+
+    // ---- rays of this wave: column col of block cb
+    const uint32_t ray0 = (tile * NW + wave) * (32 * CB);
+    uint32_t rid[CB];
+    bool valid[CB];
+    Ray ray[CB];
+    u32x4 din[KS_D0][CB];
+    u32x4 skip[KS_SK][CB];
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) {
+        const uint32_t r = ray0 + 32 * cb + col;
+        valid[cb] = r < a.total_rays;
+        rid[cb] = valid[cb] ? r : a.total_rays - 1;
+        ray[cb] = camera_ray(a, rid[cb]);
+        float ou[3], v[3];
+        unify(a, ray[cb], ou);
+        v[0] = (ou[0] - a.cx) / a.dmax;
+        v[1] = (ou[1] - a.cy) / a.dmax;
+        v[2] = (ou[2] - a.cz) / a.dmax;
+        float f[kDSlots];
+        if constexpr (DIN == kDinEncoded) {
+            fourier<5, !BF16>(v, g, f);
+            fourier<2, !BF16>(ray[cb].r, g, f + 30);
+            f[42] = g ? ray[cb].r[0] : v[0];
+            f[43] = g ? ray[cb].r[1] : v[1];
+            f[44] = g ? ray[cb].r[2] : v[2];
+            f[45] = f[46] = f[47] = 0.0f;
+#pragma unroll
+            for (int ks = 0; ks < KS_D0; ++ks) din[ks][cb] = P::pack(f + E * ks);
+        } else {
+            // Sec. 5.2's unencoded input: position k is ((o - c) + c_k r) / d_max,
+            // so its weight columns fold into those of u_c = (o - c) / d_max and
+            // of r (done once at create).  The folded layer reads
+            // [u', r, u_c] (layout.h p_feature) as fp32 fragments.
+            const float q9[9] = {v[0], v[1], v[2], ray[cb].r[0], ray[cb].r[1], ray[cb].r[2],
+                                 (ray[cb].o[0] - a.cx) / a.dmax, (ray[cb].o[1] - a.cy) / a.dmax,
+                                 (ray[cb].o[2] - a.cz) / a.dmax};
+            float q[8];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                q[e] = g ? q9[2 * e + 1] : q9[2 * e];
+                q[4 + e] = (e == 0 && g == 0) ? q9[8] : 0.0f;
+            }
+            din[0][cb] = Prec<false>::pack(q);
+            din[1][cb] = Prec<false>::pack(q + 4);
+            fourier<2, !BF16>(ray[cb].r, g, f + 30);
+        }
+        // the direction skip of the last shading layer: the same direction
+        // encoding plus the identity
+        float fs[kSkipSlots];
+#pragma unroll
+        for (int k = 0; k < 12; ++k) fs[k] = f[30 + k];
+        fs[12] = g ? 0.0f : ray[cb].r[0];
+        fs[13] = g ? 0.0f : ray[cb].r[1];
+        fs[14] = g ? 0.0f : ray[cb].r[2];
+        fs[15] = 0.0f;
+#pragma unroll
+        for (int ks = 0; ks < KS_SK; ++ks) skip[ks][cb] = P::pack(fs + E * ks);
+    }
+    lds_barrier();  // bias_s and bins_s visible
+
+    // ---- depth-oracle network
+    // Layers alternate h0 -> h1 -> h0; h0 holds the input of the next layer.
+    u32x4 h0[KS_H][CB], h1[KS_H][CB];
+    auto g0 = [&](auto K, auto C) { return h0[CV(K)][CV(C)]; };
+    auto g1 = [&](auto K, auto C) { return h1[CV(K)][CV(C)]; };
+    // six 256 -> 256 ReLU layers whose biases start at bias_l0
+    auto hidden6 = [&](const float* bias_l0) {
+        for (int l = 0; l < 3; ++l) {
+            hidden_layer<BF16, CB, KS_H>(st, g, bias_l0 + 256 * (2 * l), g0, h1);
+            hidden_layer<BF16, CB, KS_H>(st, g, bias_l0 + 256 * (2 * l + 1), g1, h0);
+        }
+    };
+    {
+        auto gin = [&](auto K, auto C) { return din[CV(K)][CV(C)]; };
+        hidden_layer<BF16, CB, KS_D0, DIN == kDinEncoded ? BF16 : false>(st, g, bias_s, gin, h0);
+    }
+    hidden6(bias_s + 256);
+    // Head of the depth network: B / 64 passes of 64 classes (32 * kRbPerPass).
+    const int npass = a.B / (32 * kRbPerPass);
+    constexpr int PASS_FRAGS = KS_H * kRbPerPass;
+    auto dump_scores = [&](int p, int R, int C, const f32x16& acc) {
+        if (a.out_scores && part == 0 && valid[C]) {
+            float* dst = a.out_scores + (size_t)rid[C] * a.B;
+            const int rowb = 32 * kRbPerPass * p + 32 * R + 4 * g;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) dst[rowb + 8 * (i / 4) + (i % 4)] = acc[i];
+        }
+    };
+    // Per ray: sample depth t, width delta and class of sample k.
+    int sel[CB][NCAP];
+    float st_t[CB][NCAP], st_d[CB][NCAP];
+    if constexpr (PLACE == kPlaceTopN) {
+        TopList<NCAP> top[CB];
+        sfor<CB>([&](auto C) { top[CV(C)].init(); });
+        // PPC passes share one chunk, so the loop steps a chunk at a time.
+        constexpr int PPC = PASS_FRAGS >= kChunkFrags ? 1 : kChunkFrags / PASS_FRAGS;
+        for (int p0 = 0; p0 < npass; p0 += PPC) {
+            sfor<PPC>([&](auto Q) {
+                constexpr int q = CV(Q);
+                const int p = p0 + q;
+                if (p < npass) {
+                    run_pass<BF16, CB, KS_H, kRbPerPass, q * PASS_FRAGS>(
+                        st, g, bias_s + 7 * 256 + 32 * kRbPerPass * p, g0, [&](auto R, auto C, const f32x16& acc) {
+                            const int rowb = 32 * kRbPerPass * p + 32 * CV(R) + 4 * g;
+#pragma unroll
+                            for (int i = 0; i < 16; ++i)
+                                top[CV(C)].push_ascending(acc[i], rowb + 8 * (i / 4) + (i % 4));
+                            dump_scores(p, CV(R), CV(C), acc);
+                        });
+                }
+            });
+        }
+        sfor<CB>([&](auto C) {
+            top[CV(C)].merge_partner();
+            top[CV(C)].ascending(a.N, sel[CV(C)]);
+        });
+    } else {
+        // Inverse-CDF placement needs every class value of the ray; B <= 128
+        // keeps them in registers (the hidden activations h1 are dead here).
+        constexpr int NPM = 128 / (32 * kRbPerPass);
+        float vals[CB][NPM][kRbPerPass][16];
+        sfor<NPM>([&](auto PI) {
+            constexpr int p = CV(PI);
+            if (p < npass) {
+                run_pass<BF16, CB, KS_H, kRbPerPass, p * PASS_FRAGS>(
+                    st, g, bias_s + 7 * 256 + 32 * kRbPerPass * p, g0, [&](auto R, auto C, const f32x16& acc) {
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) vals[CV(C)][p][CV(R)][i] = 1.0f / (1.0f + expf(-acc[i]));
+                        dump_scores(p, CV(R), CV(C), acc);
+                    });
+            } else {
+                sfor<CB>([&](auto C) {
+#pragma unroll
+                    for (int R = 0; R < kRbPerPass; ++R)
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) vals[CV(C)][p][R][i] = 0.0f;
+                });
+            }
+        });
+        sfor<CB>([&](auto C) {
+            cdf_place<NPM, NCAP>(vals[CV(C)], g, a.N, a.B, a.near, a.dmax, a.log2_span1, st_t[CV(C)],
+                                 st_d[CV(C)], sel[CV(C)]);
+        });
+    }
+    // sample k of column block cb: depth, width
+    auto sample_td = [&](int cb, int k, float& t, float& d) {
+        if constexpr (PLACE == kPlaceTopN) {
+            // Always a class index for finite scores; clamped so that no
+            // sentinel can address outside the class table.
+            const int bin = min(pick(sel[cb], k), a.B - 1);
+            t = bins_s[bin];
+            d = bins_s[a.B + bin];
+        } else {
+            t = pick_f(st_t[cb], NCAP, k);
+            d = pick_f(st_d[cb], NCAP, k);
+        }
+    };
+
+    // ---- shading network per sample, composited front to back
+    const int s_bias = 7 * 256 + a.B;
+    float T[CB], Cr[CB], Cg[CB], Cb[CB], Dp[CB];
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) T[cb] = 1.0f, Cr[cb] = Cg[cb] = Cb[cb] = Dp[cb] = 0.0f;
+
+    for (int k = k_begin; k < k_end; ++k) {
+        u32x4 sin_[KS_S0][CB];
+        float tk[CB], dk[CB];
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb) {
+            sample_td(cb, k, tk[cb], dk[cb]);
+            float x[3], w[3];
+#pragma unroll
+            for (int c = 0; c < 3; ++c) x[c] = ray[cb].o[c] + tk[cb] * ray[cb].r[c];
+            warp(a, x, w);
+            float f[kSSlots];
+            fourier<5, !BF16>(w, g, f);
+            f[30] = g ? w[2] : w[0];
+            f[31] = g ? 0.0f : w[1];
+#pragma unroll
+            for (int ks = 0; ks < KS_S0; ++ks) sin_[ks][cb] = P::pack(f + E * ks);
+        }
+        {
+            auto gs = [&](auto K, auto C) { return sin_[CV(K)][CV(C)]; };
+            hidden_layer<BF16, CB, KS_S0>(st, g, bias_s + s_bias, gs, h0);
+        }
+        hidden6(bias_s + s_bias + 256);
+        auto gh = [&](auto K, auto C) {
+            if constexpr (CV(K) < KS_H) return h0[CV(K)][CV(C)];
+            else return skip[CV(K) - KS_H][CV(C)];
+        };
+        run_pass<BF16, CB, KS_H + KS_SK, 1, 0>(
+            st, g, bias_s + s_bias + 7 * 256, gh, [&](auto R, auto C, const f32x16& acc) {
+                constexpr int cb = CV(C);
+                // lanes of group 0 hold rows 0..3 = (r, g, b, sigma) in registers 0..3
+                const float cr = 1.0f / (1.0f + expf(-acc[0]));
+                const float cg = 1.0f / (1.0f + expf(-acc[1]));
+                const float cbl = 1.0f / (1.0f + expf(-acc[2]));
+                const float sigma = fmaxf(acc[3], 0.0f);
+                const float tau = sigma * dk[cb];
+                const float alpha = -expm1f(-tau);
+                const float wgt = T[cb] * alpha;
+                Cr[cb] += wgt * cr;
+                Cg[cb] += wgt * cg;
+                Cb[cb] += wgt * cbl;
+                Dp[cb] += wgt * tk[cb];
+                T[cb] *= expf(-tau);
+            });
+    }
+    st.finish();  // no copy into LDS may outlive the workgroup
+
+    // ---- outputs (lane group 0 holds the composited values)
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) {
+        if (g == 0 && valid[cb]) {
+            if (nsplit > 1) {
+                const uint32_t local = tile_local * (32 * CB * NW) + wave * (32 * CB) + 32 * cb + col;
+                float* q = a.partial + ((size_t)local * nsplit + part) * 5;
+                q[0] = Cr[cb];
+                q[1] = Cg[cb];
+                q[2] = Cb[cb];
+                q[3] = Dp[cb];
+                q[4] = T[cb];
+            } else {
+                float* o = a.out_rgb + (size_t)rid[cb] * 3;
+                o[0] = Cr[cb];
+                o[1] = Cg[cb];
+                o[2] = Cb[cb];
+                if (a.out_depth) a.out_depth[rid[cb]] = Dp[cb];
+            }
+            if (a.out_bins && part == 0) {
+                for (int k = 0; k < a.N; ++k) a.out_bins[(size_t)rid[cb] * a.N + k] = pick(sel[cb], k);
+            }
+            if (a.out_samples && part == 0) {
+                for (int k = 0; k < a.N; ++k) {
+                    float t, d;
+                    sample_td(cb, k, t, d);
+                    a.out_samples[((size_t)rid[cb] * a.N + k) * 2 + 0] = t;
+                    a.out_samples[((size_t)rid[cb] * a.N + k) * 2 + 1] = d;
+                }
+            }
+        }
+    }
+}
+
+// One render variant; ncap selects the sample capacity.
+template <bool B16, int CB, int NW, int OCC, int PL, int DIN>
+hipError_t launch_variant(int ncap, const RenderArgs& a, dim3 grid, hipStream_t stream) {
+    if (ncap == 4)
+        hipLaunchKernelGGL((render_kernel<B16, CB, NW, OCC, 4, PL, DIN>), grid, dim3(64 * NW), 0, stream, a);
+    else if (ncap == 8)
+        hipLaunchKernelGGL((render_kernel<B16, CB, NW, OCC, 8, PL, DIN>), grid, dim3(64 * NW), 0, stream, a);
+    else
+        hipLaunchKernelGGL((render_kernel<B16, CB, NW, OCC, 16, PL, DIN>), grid, dim3(64 * NW), 0, stream, a);
+    return hipGetLastError();
+}
+
+// Both depth inputs of one precision and placement.
+template <bool B16, int CB, int NW, int OCC, int PL>
+hipError_t launch_placement(int ncap, int din, const RenderArgs& a, dim3 grid, hipStream_t stream) {
+    return din == kDinPositions ? launch_variant<B16, CB, NW, OCC, PL, kDinPositions>(ncap, a, grid, stream)
+                                : launch_variant<B16, CB, NW, OCC, PL, kDinEncoded>(ncap, a, grid, stream);
+}
+
+}  // namespace
+}  // namespace donerf

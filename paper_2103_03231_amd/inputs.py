@@ -208,6 +208,8 @@ WORKLOADS = {
     "frame400_n4_bf16": Workload("frame400_n4_bf16", 400, 400, (0, 1, 2, 3, 4), 4),
     "frame400_n4_cdf_bf16": Workload("frame400_n4_cdf_bf16", 400, 400, (0, 1, 2, 3, 4), 4,
                                      select="cdf", want_depth=True),
+    "frame400_n4_positions_bf16": Workload("frame400_n4_positions_bf16", 400, 400, (0, 1, 2, 3, 4), 4,
+                                           depth_input="positions"),
     "frame800_n8_depth_bf16": Workload("frame800_n8_depth_bf16", 800, 800, (0, 1, 2, 3, 4), 8,
                                        want_depth=True),
     "hd1080_n4_softmax_bf16": Workload("hd1080_n4_softmax_bf16", 1080, 1920, tuple(range(10)), 4,

@@ -30,7 +30,11 @@ def test_header_declarations_are_exported():
 @pytest.mark.parametrize("B", [64, 128, 192, 256])
 def test_weight_count_matches_blob(B):
     assert b.donerf_weight_count(B) == inputs.n_weights(B) == inputs.make_weights(B, 0).size
+    pos = inputs.n_weights(B, "positions")
+    assert b.donerf_weight_count(B, b.DEPTH_POSITIONS) == pos == inputs.make_weights(B, 0, "positions").size
+    assert pos - inputs.n_weights(B) == 256 * (6 + 3 * B - 90)
     assert b.donerf_weight_count(0) == 0
+    assert b.donerf_weight_count(B, 2) == 0
 
 
 def test_status_strings():
@@ -51,6 +55,7 @@ W128 = inputs.make_weights(128, 0)
     ({"n_max": 17}, b.E_INVALID_ARG),
     ({"precision": 7}, b.E_INVALID_ARG),
     ({"select": 3}, b.E_INVALID_ARG),
+    ({"depth_input": 2}, b.E_INVALID_ARG),
     ({"far": float("inf")}, b.E_NONFINITE),
     ({"centre": (0.0, float("nan"), 0.0)}, b.E_NONFINITE),
     ({"n_bins": 100}, b.E_UNSUPPORTED),
@@ -66,6 +71,10 @@ def test_create_rejects_bad_config(kw, status):
 def test_create_rejects_bad_weights():
     with pytest.raises(b.DonerfError) as e:
         b.donerf_create(b.Config(), W128[:-1])
+    assert e.value.status == b.E_SIZE
+    # the positions input needs the wider first layer
+    with pytest.raises(b.DonerfError) as e:
+        b.donerf_create(b.Config(depth_input=b.DEPTH_POSITIONS), W128)
     assert e.value.status == b.E_SIZE
     w = W128.copy()
     w[12345] = np.inf

@@ -27,9 +27,13 @@ def log(*a):
     sys.stdout.flush()
 
 
-def renderer(precision, n_bins=128, n_max=4, fov=60.0, select=b.SELECT_TOPN, seed=0):
-    w = inputs.make_weights(n_bins, seed)
-    cfg = b.Config(n_bins=n_bins, n_max=n_max, precision=PREC[precision], fov_x_deg=fov, select=select)
+DIN = {"encoded": b.DEPTH_ENCODED, "positions": b.DEPTH_POSITIONS}
+
+
+def renderer(precision, n_bins=128, n_max=4, fov=60.0, select=b.SELECT_TOPN, seed=0, depth_input="encoded"):
+    w = inputs.make_weights(n_bins, seed, depth_input)
+    cfg = b.Config(n_bins=n_bins, n_max=n_max, precision=PREC[precision], fov_x_deg=fov, select=select,
+                   depth_input=DIN[depth_input])
     return b.Renderer(cfg, w), w
 
 
@@ -40,7 +44,7 @@ def gpu_render(r, poses, H, W, N):
 
 
 def check_against_oracle(g, w, poses, H, W, N, precision, n_bins=128, fov=60.0, subset=None,
-                         max_flip_frac=0.0, label=""):
+                         max_flip_frac=0.0, label="", depth_input="encoded"):
     gb = g["bins"].reshape(-1, N)
     rgb = g["rgb"].reshape(-1, 3)
     depth = g["depth"].reshape(-1)
@@ -48,7 +52,7 @@ def check_against_oracle(g, w, poses, H, W, N, precision, n_bins=128, fov=60.0, 
     if subset is not None:
         gb, rgb, depth, scores = gb[subset], rgb[subset], depth[subset], scores[subset]
     ora = O.render(w, poses, H, W, N, n_bins=n_bins, fov_x_deg=fov, precision=precision,
-                   forced_bins=gb, ray_subset=subset)
+                   forced_bins=gb, ray_subset=subset, depth_input=depth_input)
     natural = O.topn(ora["logits"].astype(np.float32), N)
     flips = np.any(natural != gb, axis=1)
     err = np.abs(rgb - ora["rgb"]).max()
@@ -196,7 +200,8 @@ def test_render_rejects_bad_sample_count():
 def _sampled(workload, n_sample, seed=0):
     wl = inputs.WORKLOADS[workload]
     r, w = renderer(wl.precision, n_bins=wl.n_bins, n_max=wl.N, fov=wl.fov_deg,
-                    select=b.SELECT_TOPN_SOFTMAX if wl.select == "topn_softmax" else b.SELECT_TOPN)
+                    select=b.SELECT_TOPN_SOFTMAX if wl.select == "topn_softmax" else b.SELECT_TOPN,
+                    depth_input=wl.depth_input)
     poses = wl.poses()
     if wl.name.startswith("stereo"):
         poses = poses[:2]            # one stereo pair of the 60-pose sequence
@@ -217,7 +222,7 @@ def _sampled(workload, n_sample, seed=0):
          "bins": out["bins"].reshape(-1, wl.N)[sub].cpu().numpy()}
     gb = g["bins"]
     ora = O.render(w, poses, wl.H, wl.W, wl.N, n_bins=wl.n_bins, fov_x_deg=wl.fov_deg,
-                   precision=wl.precision, forced_bins=gb, ray_subset=subset)
+                   precision=wl.precision, forced_bins=gb, ray_subset=subset, depth_input=wl.depth_input)
     flips = np.any(O.topn(ora["logits"].astype(np.float32), wl.N) != gb, axis=1)
     err = np.abs(g["rgb"] - ora["rgb"]).max()
     derr = np.abs(g["depth"] - ora["depth"]).max()
@@ -230,6 +235,10 @@ def _sampled(workload, n_sample, seed=0):
 
 def test_frame400_n4_bf16_sampled():
     _sampled("frame400_n4_bf16", 3000)
+
+
+def test_frame400_n4_positions_bf16_sampled():
+    _sampled("frame400_n4_positions_bf16", 3000)
 
 
 def test_frame800_n8_depth_bf16_sampled():
@@ -375,4 +384,75 @@ def test_depth_input_features_match_oracle():
     err = np.abs(feats - ref).max()
     log(f"[depth features] maxabs {err:.3e}")
     assert err <= 2 * 2.0 ** -23, err
+    r.close()
+
+
+# ------------------------------------------------------------------ the paper's unencoded depth input
+
+def _position_probe_blob(B, cols):
+    """Depth network whose score j is input cols[j] of the 6 + 3 B: layer 0
+    copies the selected inputs shifted by +4 (kept by ReLU), identities, the
+    head removes the shift (exact in fp32 up to the shift's rounding)."""
+    n_in = 6 + 3 * B
+    W0 = np.zeros((256, n_in), np.float32)
+    W0[np.arange(len(cols)), cols] = 1.0
+    b0 = np.zeros(256, np.float32)
+    b0[:len(cols)] = 4.0
+    d = [(W0, b0)] + [(np.eye(256, dtype=np.float32), np.zeros(256, np.float32))] * 6
+    W7 = np.zeros((B, 256), np.float32)
+    W7[np.arange(len(cols)), np.arange(len(cols))] = 1.0
+    b7 = np.zeros(B, np.float32)
+    b7[:len(cols)] = -4.0
+    d.append((W7, b7))
+    s = inputs.make_weights(B, 0, "positions")[-412272:]
+    return np.concatenate([np.concatenate([W.ravel(), bb]) for W, bb in d] + [s])
+
+
+@pytest.mark.parametrize("B", [64, 128])
+def test_positions_inputs_match_oracle(B):
+    """fp32: the folded first layer reproduces the unfolded input.  Scores of
+    a selecting network read back the origin, the direction and positions of
+    the first and last classes; the oracle builds them explicitly."""
+    n_in = 6 + 3 * B
+    poses = inputs.make_poses([0, 9])
+    for cols in (np.arange(B), np.arange(n_in - B, n_in)):
+        blob = _position_probe_blob(B, cols)
+        r = b.Renderer(b.Config(n_bins=B, n_max=4, precision=b.FP32, depth_input=b.DEPTH_POSITIONS), blob)
+        g = gpu_render(r, poses, 19, 23, 4)
+        got = g["scores"].reshape(-1, B).astype(np.float64)
+        ref = O.render(blob, poses, 19, 23, 4, n_bins=B, depth_input="positions")["logits"]
+        err = np.abs(got - ref).max()
+        log(f"[positions probe B={B} cols {cols[0]}..{cols[-1]}] maxabs {err:.3e}")
+        # |input| <= 1 plus the shift of 4: a few fp32 ulp of 4
+        assert err <= 2e-6, err
+        r.close()
+
+
+@pytest.mark.parametrize("precision", ["fp32", "bf16"])
+@pytest.mark.parametrize("N,B,H,W,P,select", [
+    (4, 128, 32, 32, 1, "topn"),
+    (1, 64, 17, 23, 1, "topn"),
+    (8, 256, 16, 24, 1, "topn"),
+    (16, 192, 12, 20, 2, "topn"),
+    (4, 128, 24, 40, 1, "cdf"),
+])
+def test_positions_variants(precision, N, B, H, W, P, select):
+    sel = b.SELECT_CDF if select == "cdf" else b.SELECT_TOPN
+    r, w = renderer(precision, n_bins=B, n_max=max(N, 4), select=sel, seed=3, depth_input="positions")
+    poses = inputs.make_poses(list(range(20, 20 + P)))
+    g = gpu_render(r, poses, H, W, N)
+    label = f"positions {select} {precision} N={N} B={B} {P}x{H}x{W}"
+    if select == "cdf":
+        samp = g["samples"].reshape(-1, N, 2)
+        t_ref, _, _ = O.cdf_samples(g["scores"].reshape(-1, B), N, 0.1, 10.0)
+        cerr = np.abs(_log_coord(samp[..., 0]) - _log_coord(t_ref)).max()
+        ora = O.render(w, poses, H, W, N, n_bins=B, precision=precision, select="cdf",
+                       forced_samples=(samp[..., 0], samp[..., 1]), depth_input="positions")
+        err = np.abs(g["rgb"].reshape(-1, 3) - ora["rgb"]).max()
+        serr = np.abs(g["scores"].reshape(-1, B) - ora["logits"]).max()
+        log(f"[{label}] coord_maxabs={cerr:.3e} rgb_maxabs={err:.3e} score_maxabs={serr:.3e}")
+        assert cerr <= CDF_COORD_TOL and err <= TOL[precision]
+    else:
+        check_against_oracle(g, w, poses, H, W, N, precision, n_bins=B, label=label,
+                             max_flip_frac=0.0 if precision == "fp32" else 0.03, depth_input="positions")
     r.close()
