@@ -31,8 +31,8 @@ HBM_PEAK_GBS = 8000.0
 # render_kernel_frame400_n4_bf16_traffic.md) scaled by the same counters on a
 # plain 256 MiB copy (FETCH_SIZE reads half the bytes moved: x2; WRITE_SIZE
 # exact: x1).  Valid only for the kernel sources they were taken on.
-MEASURED_TRAFFIC = {"sources_sha256_16": "21c89448c12e560c", "workload": "frame400_n4_bf16",
-                    "fetch_kib": 7332.5 * 2, "write_kib": 11760.0}
+MEASURED_TRAFFIC = {"sources_sha256_16": "94017e4f7e55b4c5", "workload": "frame400_n4_bf16",
+                    "fetch_kib": 7338.9 * 2, "write_kib": 11760.0}
 # the sources the bf16 top-N render kernel is built from
 KERNEL_SOURCES = ("paper_2103_03231_amd/csrc/render_kernel.h", "paper_2103_03231_amd/csrc/render_bf16_topn.hip",
                   "paper_2103_03231_amd/csrc/layout.h", "paper_2103_03231_amd/csrc/internal.h")
