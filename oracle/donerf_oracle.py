@@ -27,7 +27,7 @@ oracle rounds to bf16 (round-to-nearest-even) exactly where a bf16 network
 does: weights, encoded features and each hidden activation after bias + ReLU
 (the unencoded positions input is not rounded).
 Values are first rounded to fp32 and then to bf16.  Logits and head outputs
-stay unrounded.
+stay unrounded.  ``precision='fp8'`` is the mixed network of ``mlp_fp8``.
 
 Readings where the paper is silent are listed in the design document; each
 function names the one it uses.
@@ -62,6 +62,48 @@ def round_bf16(x) -> np.ndarray:
     if nan.any():
         out = np.where(nan, f, out)
     return out.astype(np.float64)
+
+
+E4M3_MAX = 448.0
+
+
+def round_e4m3(x) -> np.ndarray:
+    """Round to the OCP fp8 E4M3 grid (1 sign, 4 exponent bits with bias 7,
+    3 mantissa bits; subnormals of quantum 2^-9; largest finite 448), round to
+    nearest, ties to even.  Defined for |x| <= 448 (values are clamped before
+    they are rounded).  Returned as float64 holding the fp8 value."""
+    x = np.asarray(x, dtype=np.float64)
+    if np.any(np.abs(x) > E4M3_MAX):
+        raise ValueError("round_e4m3: |x| > 448")
+    a = np.abs(x)
+    with np.errstate(divide="ignore"):
+        e = np.floor(np.log2(np.where(a > 0, a, 1.0)))
+    # quantum: 2^(e - 3) for normal values (e >= -6), 2^-9 below
+    q = np.exp2(np.maximum(e, -6.0) - 3.0)
+    # np.rint rounds half to even; an even multiple of the quantum is an even code
+    return np.sign(x) * np.rint(a / q) * q
+
+
+def fp8_weight_scale(W) -> int:
+    """Per-layer power-of-two scale of the fp8 weights: the largest integer s
+    with max|W| 2^s <= 448, or 0 for an all-zero layer."""
+    m = float(np.max(np.abs(np.asarray(W, dtype=np.float64)))) if np.size(W) else 0.0
+    if m == 0.0:
+        return 0
+    s = int(math.floor(math.log2(E4M3_MAX / m)))
+    while m * 2.0 ** (s + 1) <= E4M3_MAX:
+        s += 1
+    while m * 2.0 ** s > E4M3_MAX:
+        s -= 1
+    return s
+
+
+def quantize_fp8_weights(W) -> np.ndarray:
+    """fp8 weights as the network uses them: W 2^s rounded to E4M3 (from the
+    fp32 value), times 2^-s."""
+    W32 = np.asarray(W, dtype=np.float64).astype(F32).astype(np.float64)
+    s = fp8_weight_scale(W32)
+    return round_e4m3(W32 * 2.0 ** s) * 2.0 ** -s
 
 
 # ---------------------------------------------------------------- depth bins
@@ -219,7 +261,10 @@ def mlp(layers, x, precision="fp64", skip=None, round_input=True):
     output is returned without activation.  ``skip`` (rows x s) is appended to
     the last layer's input (App. D's single direction skip).  x is (rows, in).
     In bf16 mode weights, inputs (unless ``round_input`` is false) and hidden
-    activations are rounded to bf16; sums accumulate in fp64."""
+    activations are rounded to bf16; sums accumulate in fp64.  fp8 mode:
+    ``mlp_fp8``."""
+    if precision == "fp8":
+        return mlp_fp8(layers, x, skip, round_input)
     rb = round_bf16 if precision == "bf16" else (lambda a: np.asarray(a, dtype=np.float64))
     h = rb(x) if round_input else np.asarray(x, dtype=np.float64)
     n = len(layers)
@@ -249,6 +294,29 @@ def depth_positions_input(o, r, ou, centre, d_max, centres):
     x = sample_points(o, r, np.broadcast_to(cen[None, :], (o.shape[0], cen.size))).astype(F32)
     p = ((x - c) / d_max).astype(F32)
     return np.concatenate([v, r.astype(F32), p.reshape(o.shape[0], -1)], axis=1)
+
+
+def mlp_fp8(layers, x, skip=None, round_input=True):
+    """The mixed fp8 network.  The paper leaves lower bit widths as future
+    headroom (Sec. 6.1) and fixes no scheme; this one keeps the first and the
+    last layer in bf16 (weights, inputs and skip rounded to bf16) and runs
+    the hidden layers in fp8: weights by ``quantize_fp8_weights``, inputs in
+    E4M3.  Each activation after bias and ReLU is clamped to 448 and rounded
+    to E4M3 where an fp8 layer reads it; where the last layer reads it, it is
+    rounded to bf16 (no clamp).  Sums accumulate in fp64."""
+    n = len(layers)
+    h = round_bf16(x) if round_input else np.asarray(x, dtype=np.float64)
+    for li, (W, b) in enumerate(layers):
+        if li == n - 1 and skip is not None:
+            h = np.concatenate([h, round_bf16(skip)], axis=1)
+        Wq = round_bf16(W) if li in (0, n - 1) else quantize_fp8_weights(W)
+        y = h @ Wq.T + b
+        if li < n - 1:
+            r = np.maximum(y, 0.0)
+            h = round_bf16(r) if li == n - 2 else round_e4m3(np.minimum(r, E4M3_MAX))
+        else:
+            h = y
+    return h
 
 
 # ---------------------------------------------------------------- selection
