@@ -53,8 +53,15 @@ typedef enum donerf_status {
 
 typedef enum donerf_precision {
     DONERF_FP32 = 0, /* fp32 weights, features and activations, fp32 MFMA    */
-    DONERF_BF16 = 1  /* bf16 weights, features and hidden activations (RNE),
+    DONERF_BF16 = 1, /* bf16 weights, features and hidden activations (RNE),
                         fp32 accumulation, fp32 scores, heads, compositing   */
+    DONERF_FP8 = 2   /* the lower bit width Sec. 6.1 leaves as headroom: the
+                        six hidden layers of each network in OCP E4M3 (weights
+                        W 2^s rounded to nearest even with the largest s that
+                        keeps max|W| 2^s <= 448, one s per layer; their inputs
+                        clamped to [0, 448] after ReLU and rounded to E4M3);
+                        the first layers and heads as in DONERF_BF16, fp32
+                        accumulation throughout                               */
 } donerf_precision;
 
 typedef enum donerf_select {

@@ -27,6 +27,7 @@ E_UNSUPPORTED = -7
 
 FP32 = 0
 BF16 = 1
+FP8 = 2
 SELECT_TOPN = 0
 SELECT_TOPN_SOFTMAX = 1
 SELECT_CDF = 2

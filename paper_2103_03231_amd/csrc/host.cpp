@@ -16,7 +16,8 @@ using namespace donerf;
 
 struct donerf_handle {
     donerf_cfg cfg;
-    bool bf16;
+    int prec;            // layout.h Precision of the network
+    int32_t wscale[16];  // per streamed layer: E8M0 scale of fp8 weights (127 - s), else 127
     int device;
     hipStream_t stream;
     void* d_frags;       // device: depth stream then shading stream
@@ -74,7 +75,7 @@ int validate_cfg(const donerf_cfg* c) {
     if (c->n_max < 1 || c->n_max > DONERF_MAX_SAMPLES)
         return fail(DONERF_E_INVALID_ARG, "n_max must lie in [1, 16]");
     if (c->n_max > c->n_bins) return fail(DONERF_E_INVALID_ARG, "n_max exceeds n_bins");
-    if (c->precision != DONERF_FP32 && c->precision != DONERF_BF16)
+    if (c->precision != DONERF_FP32 && c->precision != DONERF_BF16 && c->precision != DONERF_FP8)
         return fail(DONERF_E_INVALID_ARG, "unknown precision");
     if (c->select != DONERF_SELECT_TOPN && c->select != DONERF_SELECT_TOPN_SOFTMAX &&
         c->select != DONERF_SELECT_CDF)
@@ -112,6 +113,41 @@ uint16_t to_bf16(float x) {  // round to nearest even (inputs are finite)
     std::memcpy(&u, &x, 4);
     u += 0x7fffu + ((u >> 16) & 1u);
     return (uint16_t)(u >> 16);
+}
+
+// OCP E4M3 code of x, |x| <= 448: round to nearest, ties to even, on the
+// grid of 3 mantissa bits.  Code bits: sign, 4 exponent bits (bias 7),
+// 3 mantissa bits; exponent field 0 holds the subnormals m 2^-9.
+uint8_t to_e4m3(float x) {
+    const double a = std::fabs((double)x);
+    const uint8_t sign = std::signbit(x) ? 0x80 : 0x00;
+    int E = 0;
+    std::frexp(a, &E);                  // a = f 2^E, f in [0.5, 1): binade e = E - 1
+    const int e = E - 1;
+    if (a == 0.0 || e < -6) {
+        // n 2^-9 with n = 0..8; n = 8 is 2^-6, whose code 0x08 is the
+        // smallest normal, so the code is n itself
+        return (uint8_t)(sign | (uint8_t)std::nearbyint(std::ldexp(a, 9)));
+    }
+    int n = (int)std::nearbyint(std::ldexp(a, 3 - e));   // 8..16, ties to even
+    int ee = e;
+    if (n == 16) {
+        n = 8;
+        ++ee;
+    }
+    return (uint8_t)(sign | (uint8_t)((ee + 7) << 3) | (uint8_t)(n - 8));
+}
+
+// Largest s with max|W| 2^s <= 448 (0 for an all-zero layer): the per-layer
+// power-of-two scale of fp8 weights.
+int fp8_scale(const float* W, size_t n) {
+    double m = 0.0;
+    for (size_t k = 0; k < n; ++k) m = std::fmax(m, std::fabs((double)W[k]));
+    if (m == 0.0) return 0;
+    int s = (int)std::floor(std::log2(448.0 / m));
+    while (std::ldexp(m, s + 1) <= 448.0) ++s;
+    while (std::ldexp(m, s) > 448.0) --s;
+    return s;
 }
 
 float bf16_value(float x) {
@@ -154,49 +190,56 @@ std::vector<float> fold_positions_layer(const float* W, int B, bool bf16, const 
     return out;
 }
 
-// Logical input column of the blob for K step ks, lane group g, element e.
-int in_col(bool bf16, int kind, int ks, int g, int e) {
-    const int E = elems(bf16);
+// Logical input column of the blob for K step ks, lane group g, element e of
+// a layer whose steps have precision p.
+int in_col(int p, int kind, int ks, int g, int e) {
+    const int E = elems(p);
     switch (kind) {
         case kDFirst: return d_feature(g, ks * E + e);
         case kDFirstPos: return p_feature(ks, g, e);
         case kSFirst: return s_feature(g, ks * E + e);
         case kHiddenL:
-        case kDHead: return chained_row(bf16, ks, g, e);
+        case kDHead: return chained_row(p, ks, g, e);
         default: {  // kSHead: chained hidden units, then the direction skip
-            const int ksh = ksteps(bf16, kHidden);
-            if (ks < ksh) return chained_row(bf16, ks, g, e);
+            const int ksh = ksteps(p, kHidden);
+            if (ks < ksh) return chained_row(p, ks, g, e);
             const int f = skip_feature(g, (ks - ksh) * E + e);
             return f < 0 ? -1 : kHidden + f;
         }
     }
 }
 
-// Append one layer's fragments, in the order the kernel consumes them
-// (pass, K step, row block within the pass), padded to whole chunks.
-void pack_layer(bool bf16, int kind, int n_bins, const float* W, std::vector<uint8_t>& dst) {
+// Append one layer's steps, in the order the kernel consumes them (pass,
+// K step, row block within the pass), padded to whole chunks.  prec: the
+// layer's step precision (layout.h frag_prec); net: the network's (for the
+// chunk count); s: power-of-two scale of fp8 weights (W 2^s is rounded).
+void pack_layer(int prec, int net, int kind, int n_bins, const float* W, int s, std::vector<uint8_t>& dst) {
     const LayerGeom lg = layer_geom(kind, n_bins);
-    const int KS = ksteps(bf16, lg.kpad);
-    const int E = elems(bf16);
+    const int KS = ksteps(prec, lg.kpad);
+    const int E = elems(prec), EB = elem_bytes(prec), U = units(prec);
     const size_t start = dst.size();
-    dst.resize(start + (size_t)layer_chunks(bf16, kind, n_bins) * kChunkBytes, 0);
+    dst.resize(start + (size_t)layer_chunks(net, kind, n_bins) * kChunkBytes, 0);
     uint8_t* out = dst.data() + start;
     size_t f = 0;
     for (int p = 0; p < lg.rb / lg.rbp; ++p)
         for (int ks = 0; ks < KS; ++ks)
             for (int r = 0; r < lg.rbp; ++r, ++f) {
                 const int rb = p * lg.rbp + r;
-                uint8_t* frag = out + f * kFragBytes;
+                uint8_t* step = out + f * U * kFragBytes;
                 for (int lane = 0; lane < 64; ++lane) {
                     const int row = 32 * rb + lane % 32, g = lane / 32;
                     for (int e = 0; e < E; ++e) {
-                        const int colx = in_col(bf16, kind, ks, g, e);
+                        const int colx = in_col(prec, kind, ks, g, e);
                         const float v = (row < lg.out_rows && colx >= 0) ? W[(size_t)row * lg.in_cols + colx] : 0.0f;
-                        if (bf16) {
+                        // element e: unit (e * EB) / 16, byte (e * EB) % 16 of the lane's 16
+                        uint8_t* dstp = step + ((e * EB) / 16) * kFragBytes + lane * 16 + (e * EB) % 16;
+                        if (prec == kFP8) {
+                            *dstp = to_e4m3((float)std::ldexp((double)v, s));
+                        } else if (prec == kBF16) {
                             const uint16_t h = to_bf16(v);
-                            std::memcpy(frag + lane * 16 + e * 2, &h, 2);
+                            std::memcpy(dstp, &h, 2);
                         } else {
-                            std::memcpy(frag + lane * 16 + e * 4, &v, 4);
+                            std::memcpy(dstp, &v, 4);
                         }
                     }
                 }
@@ -281,7 +324,7 @@ int render_impl(donerf_t* h, const float* poses, int32_t P, int32_t H, int32_t W
         // last, partial round are split by samples over up to n_cu / r
         // workgroups each (every part recomputes the depth network), and a
         // combine pass composites the parts.
-        const uint32_t rpb = (uint32_t)rays_per_block(h->bf16);
+        const uint32_t rpb = (uint32_t)rays_per_block(h->prec);
         const uint32_t tiles = (a.total_rays + rpb - 1) / rpb;
         const uint32_t round = (uint32_t)h->n_cu;
         const uint32_t full = tiles / round * round, rem = tiles - full;
@@ -291,12 +334,13 @@ int render_impl(donerf_t* h, const float* poses, int32_t P, int32_t H, int32_t W
         a.n_full = split > 1 ? full : tiles;
         a.split = (int32_t)split;
         a.partial = h->partial;
-        hipError_t e = launch_render(h->bf16, ncap_for(N), place,
+        std::memcpy(a.wscale, h->wscale, sizeof a.wscale);
+        hipError_t e = launch_render(h->prec, ncap_for(N), place,
                                      c.depth_input == DONERF_DEPTH_POSITIONS ? kDinPositions : kDinEncoded, a,
                                      split > 1 ? rem : 0, h->stream);
         if (e != hipSuccess) return hip_fail(e, "render launch");
         if (split > 1) {
-            e = launch_combine(h->bf16, a, h->stream);
+            e = launch_combine(h->prec, a, h->stream);
             if (e != hipSuccess) return hip_fail(e, "combine launch");
         }
         if (out_scores && c.select == DONERF_SELECT_TOPN_SOFTMAX) {
@@ -336,7 +380,7 @@ int donerf_create(const donerf_cfg* cfg, const float* weights, size_t n_weights,
     rc = check_device(&dev);
     if (rc) return rc;
 
-    const bool bf16 = cfg->precision == DONERF_BF16;
+    const int prec = cfg->precision == DONERF_FP8 ? kFP8 : cfg->precision == DONERF_BF16 ? kBF16 : kF32;
     const int B = cfg->n_bins;
     const bool positions = cfg->depth_input == DONERF_DEPTH_POSITIONS;
     std::vector<float> bounds, centres, widths;
@@ -344,17 +388,24 @@ int donerf_create(const donerf_cfg* cfg, const float* weights, size_t n_weights,
     std::vector<uint8_t> frags;
     std::vector<float> bias;
     int n_d_chunks = 0, n_s_chunks = 0;
+    int32_t wscale[16];
     size_t off = 0;
     for (int l = 0; l < 16; ++l) {
         const int kind = (l == 0 && positions) ? kDFirstPos : kKinds[l];
         const LayerGeom lg = layer_geom(kind, B);
+        const int fp = frag_prec(prec, kind);
+        const int s = fp == kFP8 ? fp8_scale(weights + off, blob_w_count(l, B, cfg->depth_input)) : 0;
+        wscale[l] = 127 - s;
         if (kind == kDFirstPos) {
-            const std::vector<float> folded = fold_positions_layer(weights + off, B, bf16, centres, cfg->far_dist);
-            pack_layer(false, kind, B, folded.data(), frags);
+            // the folded sums use the weights as the first layer of the
+            // network uses them: bf16 in bf16 and fp8 networks
+            const std::vector<float> folded =
+                fold_positions_layer(weights + off, B, prec != kF32, centres, cfg->far_dist);
+            pack_layer(fp, prec, kind, B, folded.data(), 0, frags);
         } else {
-            pack_layer(bf16, kind, B, weights + off, frags);
+            pack_layer(fp, prec, kind, B, weights + off, s, frags);
         }
-        (l < 8 ? n_d_chunks : n_s_chunks) += layer_chunks(bf16, kind, B);
+        (l < 8 ? n_d_chunks : n_s_chunks) += layer_chunks(prec, kind, B);
         off += blob_w_count(l, B, cfg->depth_input);
         const size_t b0 = bias.size();
         bias.resize(b0 + bias_len(kind, B), 0.0f);
@@ -365,7 +416,8 @@ int donerf_create(const donerf_cfg* cfg, const float* weights, size_t n_weights,
     donerf_t* h = new (std::nothrow) donerf_handle();
     if (!h) return fail(DONERF_E_NOMEM, "host allocation failed");
     h->cfg = *cfg;
-    h->bf16 = bf16;
+    h->prec = prec;
+    std::memcpy(h->wscale, wscale, sizeof wscale);
     h->device = dev;
     h->stream = nullptr;
     h->n_d_chunks = n_d_chunks;
@@ -435,7 +487,7 @@ int donerf_debug_topn(donerf_t* h, const float* scores, int32_t rays, int32_t N,
     if (!scores || !out_idx) return fail(DONERF_E_INVALID_ARG, "NULL buffer");
     if (rays < 1) return fail(DONERF_E_INVALID_ARG, "rays must be >= 1");
     if (N < 1 || N > h->cfg.n_max || N > h->cfg.n_bins) return fail(DONERF_E_INVALID_ARG, "N out of range");
-    hipError_t e = launch_topn(h->bf16, ncap_for(N), scores, rays, N, h->cfg.n_bins, out_idx, h->stream);
+    hipError_t e = launch_topn(h->prec != kF32, ncap_for(N), scores, rays, N, h->cfg.n_bins, out_idx, h->stream);
     if (e != hipSuccess) return hip_fail(e, "topn launch");
     return DONERF_OK;
 }

@@ -40,6 +40,8 @@ struct RenderArgs {
     float near;             // d_min
     float dmax;             // d_max
     float log2_span1;       // log2(d_max - d_min + 1), for the inverse of Eq. 3
+    int32_t wscale[16];     // per streamed layer (depth 0-7, shading 8-15): E8M0 scale of
+                            // its fp8 weights, 127 - s for weights stored as W 2^s
     float poses[kMaxPosesPerLaunch][12];
 };
 
@@ -58,21 +60,24 @@ constexpr int kBf16CB = DONERF_BF16_CB;
 constexpr int kBf16NW = DONERF_BF16_NW;
 constexpr int kBf16Occ = DONERF_BF16_OCC;
 
-// Rays handled by one workgroup.
-inline int rays_per_block(bool bf16) { return bf16 ? kBf16NW * 32 * kBf16CB : 4 * 32; }
+// Rays handled by one workgroup (prec: layout.h Precision of the network;
+// the fp8 kernel has the bf16 kernel's launch shape).
+inline int rays_per_block(int prec) { return prec != kF32 ? kBf16NW * 32 * kBf16CB : 4 * 32; }
 
 // Launches a.n_full whole tiles plus n_split_tiles tiles split a.split ways.
 // place: layout.h Placement; din: layout.h DepthInput.
-hipError_t launch_render(bool bf16, int ncap, int place, int din, const RenderArgs& a, uint32_t n_split_tiles,
+hipError_t launch_render(int prec, int ncap, int place, int din, const RenderArgs& a, uint32_t n_split_tiles,
                          hipStream_t stream);
 // The variants of one precision and placement (render_*.hip).
 hipError_t launch_render_bf16_topn(int ncap, int din, const RenderArgs& a, dim3 grid, hipStream_t stream);
 hipError_t launch_render_bf16_cdf(int ncap, int din, const RenderArgs& a, dim3 grid, hipStream_t stream);
 hipError_t launch_render_fp32_topn(int ncap, int din, const RenderArgs& a, dim3 grid, hipStream_t stream);
 hipError_t launch_render_fp32_cdf(int ncap, int din, const RenderArgs& a, dim3 grid, hipStream_t stream);
+hipError_t launch_render_fp8_topn(int ncap, int din, const RenderArgs& a, dim3 grid, hipStream_t stream);
+hipError_t launch_render_fp8_cdf(int ncap, int din, const RenderArgs& a, dim3 grid, hipStream_t stream);
 // Composites the split parts of rays [n_full * rays_per_block, total_rays)
 // into out_rgb / out_depth.
-hipError_t launch_combine(bool bf16, const RenderArgs& a, hipStream_t stream);
+hipError_t launch_combine(int prec, const RenderArgs& a, hipStream_t stream);
 hipError_t launch_softmax_rows(float* scores, uint32_t rows, int B, hipStream_t stream);
 hipError_t launch_topn(bool bf16_layout, int ncap, const float* scores, int32_t rays,
                        int32_t N, int32_t B, int32_t* out_idx, hipStream_t stream);

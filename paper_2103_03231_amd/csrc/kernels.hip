@@ -74,18 +74,21 @@ __global__ void __launch_bounds__(256) topn_kernel(const float* scores, int32_t 
 
 }  // namespace
 
-hipError_t launch_render(bool bf16, int ncap, int place, int din, const RenderArgs& a, uint32_t n_split_tiles,
+hipError_t launch_render(int prec, int ncap, int place, int din, const RenderArgs& a, uint32_t n_split_tiles,
                          hipStream_t stream) {
     const dim3 grid(a.n_full + n_split_tiles * (uint32_t)a.split);
-    if (bf16)
+    if (prec == kFP8)
+        return place == kPlaceCdf ? launch_render_fp8_cdf(ncap, din, a, grid, stream)
+                                  : launch_render_fp8_topn(ncap, din, a, grid, stream);
+    if (prec == kBF16)
         return place == kPlaceCdf ? launch_render_bf16_cdf(ncap, din, a, grid, stream)
                                   : launch_render_bf16_topn(ncap, din, a, grid, stream);
     return place == kPlaceCdf ? launch_render_fp32_cdf(ncap, din, a, grid, stream)
                               : launch_render_fp32_topn(ncap, din, a, grid, stream);
 }
 
-hipError_t launch_combine(bool bf16, const RenderArgs& a, hipStream_t stream) {
-    const uint32_t first = a.n_full * (uint32_t)rays_per_block(bf16);
+hipError_t launch_combine(int prec, const RenderArgs& a, hipStream_t stream) {
+    const uint32_t first = a.n_full * (uint32_t)rays_per_block(prec);
     const uint32_t n = a.total_rays - first;
     hipLaunchKernelGGL(combine_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, a.partial, a.split, first,
                        a.total_rays, a.out_rgb, a.out_depth);

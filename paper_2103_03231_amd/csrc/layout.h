@@ -3,13 +3,18 @@
 //
 // Networks run in the transposed form Y^T = W X^T: weights are the MFMA A
 // operand (rows = output units), activations the B operand (columns = rays or
-// samples).  A "fragment" is the A operand of one MFMA step for 32 output rows:
+// samples).  One MFMA step covers 32 output rows:
 //   bf16: v_mfma_f32_32x32x16_bf16, 32 rows x 16 K; lane l holds row l%32 and
 //         K slots 8*(l/32) + e, e = 0..7 (16 bytes)
 //   fp32: four v_mfma_f32_32x32x2_f32, 32 rows x 8 K; lane l holds row l%32,
 //         sub-step e = 0..3 reads K slot 2*e + l/32 (16 bytes)
-// Each fragment is stored as 64 lanes x 16 bytes = 1 KiB, so one
-// ds_read_b128 per lane fetches it without bank conflicts.
+//   fp8:  v_mfma_scale_f32_32x32x64_f8f6f4 on E4M3, 32 rows x 64 K; lane l
+//         holds row l%32 and 32 K elements (32 bytes).  A and B place K the
+//         same way, so element e of lane group g of A multiplies element e of
+//         lane group g of B, whatever K the hardware assigns to it.
+// A step's A operand is stored as 1 KiB units of 64 lanes x 16 bytes (one
+// unit for fp32 and bf16, two for fp8: bytes 0-15 then 16-31 of each lane),
+// so one ds_read_b128 per lane and unit fetches it without bank conflicts.
 //
 // Chaining.  The fp32 accumulator of a 32x32 MFMA block holds, on lane l
 // with g = l/32, register i = 0..15 for row 8*(i/4) + 4*g + i%4 of the block
@@ -36,35 +41,36 @@ constexpr int kFragBytes = 1024;
 #ifndef DONERF_CHUNK_FRAGS
 #define DONERF_CHUNK_FRAGS 32
 #endif
-#ifndef DONERF_RING
-#define DONERF_RING 3
-#endif
 constexpr int kChunkFrags = DONERF_CHUNK_FRAGS;  // fragments per streamed chunk
 constexpr int kChunkBytes = kChunkFrags * kFragBytes;
-constexpr int kRing = DONERF_RING;               // LDS chunk slots (prefetch distance kRing - 1)
-constexpr int kWaves = 4;
-constexpr int kThreads = 64 * kWaves;
+
 constexpr int kMaxPosesPerLaunch = 32;
 #ifndef DONERF_RB_PER_PASS
 #define DONERF_RB_PER_PASS 2
 #endif
 constexpr int kRbPerPass = DONERF_RB_PER_PASS;  // 32-row blocks per accumulator pass
 
-// Elements per lane per fragment and K per fragment.
-DN_HD constexpr int elems(bool bf16) { return bf16 ? 8 : 4; }
-DN_HD constexpr int kper(bool bf16) { return bf16 ? 16 : 8; }
-// K slot within a fragment of element e on lane group g.
-DN_HD constexpr int kslot(bool bf16, int g, int e) { return bf16 ? 8 * g + e : 2 * e + g; }
+// Arithmetic of a layer's MFMA steps (bool true/false convert to bf16/fp32).
+enum Precision { kF32 = 0, kBF16 = 1, kFP8 = 2 };
+
+// K elements per lane per step, K per step, 1 KiB units per step, bytes per
+// element.
+DN_HD constexpr int elems(int p) { return p == kFP8 ? 32 : p == kBF16 ? 8 : 4; }
+DN_HD constexpr int kper(int p) { return p == kFP8 ? 64 : p == kBF16 ? 16 : 8; }
+DN_HD constexpr int units(int p) { return p == kFP8 ? 2 : 1; }
+DN_HD constexpr int elem_bytes(int p) { return p == kFP8 ? 1 : p == kBF16 ? 2 : 4; }
 // Number of K steps for a padded K.
-DN_HD constexpr int ksteps(bool bf16, int kpad) { return kpad / kper(bf16); }
+DN_HD constexpr int ksteps(int p, int kpad) { return kpad / kper(p); }
 
 // Hidden unit (logical row of the previous layer) that feeds K step ks,
 // lane group g, element e when the previous layer's accumulators are chained.
-DN_HD constexpr int chained_row(bool bf16, int ks, int g, int e) {
-    // K steps per 32-row block: 2 (bf16) or 4 (fp32)
-    return 32 * (ks / (16 / elems(bf16))) +
-           8 * (((ks % (16 / elems(bf16))) * elems(bf16) + e) / 4) + 4 * g +
-           (((ks % (16 / elems(bf16))) * elems(bf16) + e) % 4);
+// bf16 / fp32: a 32-row block feeds 2 / 4 K steps.  fp8: a K step takes the
+// 16 registers of two consecutive blocks, elements 0-15 from the first.
+DN_HD constexpr int chained_row(int p, int ks, int g, int e) {
+    return p == kFP8 ? 32 * (2 * ks + e / 16) + 8 * ((e % 16) / 4) + 4 * g + e % 4
+                     : 32 * (ks / (16 / elems(p))) +
+                           8 * (((ks % (16 / elems(p))) * elems(p) + e) / 4) + 4 * g +
+                           (((ks % (16 / elems(p))) * elems(p) + e) % 4);
 }
 
 // Per-lane feature slots.  Each column's features are split between lane
@@ -146,16 +152,22 @@ DN_HD constexpr LayerGeom layer_geom(int kind, int n_bins) {
          :                    LayerGeom{kSOut, kHidden + kSkip, kHidden + kSkipKPad, 1, 1};
 }
 
-// Whether a layer's fragments are bf16 in a network of the given precision
-// (the folded positions layer is fp32 in both).
-DN_HD constexpr bool frag_bf16(bool bf16, int kind) { return kind == kDFirstPos ? false : bf16; }
-
-// Fragments a layer streams (before padding to whole chunks).
-DN_HD constexpr int layer_frags(bool bf16, int kind, int n_bins) {
-    return layer_geom(kind, n_bins).rb * ksteps(frag_bf16(bf16, kind), layer_geom(kind, n_bins).kpad);
+// Arithmetic of a layer in a network of precision net: the folded positions
+// layer is fp32 in every network; an fp8 network keeps its first layers and
+// heads in bf16 and runs the hidden layers in fp8.
+DN_HD constexpr int frag_prec(int net, int kind) {
+    return kind == kDFirstPos ? kF32 : net != kFP8 ? net : kind == kHiddenL ? kFP8 : kBF16;
 }
-DN_HD constexpr int layer_chunks(bool bf16, int kind, int n_bins) {
-    return (layer_frags(bf16, kind, n_bins) + kChunkFrags - 1) / kChunkFrags;
+
+// 1 KiB units a layer streams (before padding to whole chunks).
+DN_HD constexpr int layer_frags(int net, int kind, int n_bins) {
+    return layer_geom(kind, n_bins).rb * ksteps(frag_prec(net, kind), layer_geom(kind, n_bins).kpad) *
+           units(frag_prec(net, kind));
+}
+// Chunks a layer streams: padded with zeros to an even number, so that every
+// layer starts in the same slot of the two-slot LDS stream.
+DN_HD constexpr int layer_chunks(int net, int kind, int n_bins) {
+    return (layer_frags(net, kind, n_bins) + 2 * kChunkFrags - 1) / (2 * kChunkFrags) * 2;
 }
 
 // Bias table: every layer's bias padded to 32 * rb floats, depth layers

@@ -6,7 +6,7 @@
 namespace donerf {
 
 hipError_t launch_render_bf16_topn(int ncap, int din, const RenderArgs& a, dim3 grid, hipStream_t stream) {
-    return launch_placement<true, kBf16CB, kBf16NW, kBf16Occ, kPlaceTopN>(ncap, din, a, grid, stream);
+    return launch_placement<kBF16, kBf16CB, kBf16NW, kBf16Occ, kPlaceTopN>(ncap, din, a, grid, stream);
 }
 
 }  // namespace donerf

@@ -6,7 +6,7 @@
 namespace donerf {
 
 hipError_t launch_render_fp32_topn(int ncap, int din, const RenderArgs& a, dim3 grid, hipStream_t stream) {
-    return launch_placement<false, 1, 4, 1, kPlaceTopN>(ncap, din, a, grid, stream);
+    return launch_placement<kF32, 1, 4, 1, kPlaceTopN>(ncap, din, a, grid, stream);
 }
 
 }  // namespace donerf

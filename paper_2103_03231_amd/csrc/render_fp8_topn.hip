@@ -1,0 +1,11 @@
+// render_fp8_topn.hip - render kernels with mixed fp8 networks (bf16 first and
+// head layers, fp8 hidden layers) and top-N placement, both depth-network inputs.
+#include "render_kernel.h"
+
+namespace donerf {
+
+hipError_t launch_render_fp8_topn(int ncap, int din, const RenderArgs& a, dim3 grid, hipStream_t stream) {
+    return launch_placement<kFP8, kBf16CB, kBf16NW, kBf16Occ, kPlaceTopN>(ncap, din, a, grid, stream);
+}
+
+}  // namespace donerf

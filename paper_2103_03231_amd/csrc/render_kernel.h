@@ -11,7 +11,7 @@
 //
 // Work split (bf16): 8 waves per workgroup, two per SIMD, one workgroup per
 // CU.  Each wave owns 32 * CB rays (the MFMA columns); the workgroup shares
-// one stream of weight fragments through a ring of kRing LDS chunks, so each
+// one stream of weight fragments through two LDS chunk slots, so each
 // weight byte read from L2 feeds every wave.  Activations never leave the
 // registers: accumulators of layer l become, after bias, ReLU and rounding,
 // the B operand of layer l+1 (layout.h explains the K permutation that makes
@@ -37,6 +37,7 @@ typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x8 __attribute__((ext_vector_type(8)));
 
 // ------------------------------------------------------------------ compile-time loops
 
@@ -57,16 +58,17 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
 }
 
-template <bool BF16>
+template <int PR>
 struct Prec;
 
 template <>
-struct Prec<true> {
-    static constexpr int E = 8;      // K elements per lane per fragment
+struct Prec<kBF16> {
+    static constexpr int E = 8;      // K elements per lane per step
+    static constexpr int U = 1;      // 1 KiB units (u32x4 per lane) per step, A and B alike
     static constexpr int KSPB = 2;   // K steps produced per 32-row block
-    __device__ static __forceinline__ f32x16 mma(u32x4 a, u32x4 b, f32x16 c) {
-        return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
-                                                       __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+    __device__ static __forceinline__ f32x16 mma(const u32x4* a, const u32x4* b, f32x16 c, int) {
+        return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a[0]),
+                                                       __builtin_bit_cast(bf16x8, b[0]), c, 0, 0, 0);
     }
     __device__ static __forceinline__ u32x4 pack(const float* f) {
         return u32x4{pack_bf16x2(f[0], f[1]), pack_bf16x2(f[2], f[3]),
@@ -75,19 +77,36 @@ struct Prec<true> {
 };
 
 template <>
-struct Prec<false> {
+struct Prec<kF32> {
     static constexpr int E = 4;
+    static constexpr int U = 1;
     static constexpr int KSPB = 4;
-    __device__ static __forceinline__ f32x16 mma(u32x4 a, u32x4 b, f32x16 c) {
-        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
-        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
-        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
-        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
+    __device__ static __forceinline__ f32x16 mma(const u32x4* a, const u32x4* b, f32x16 c, int) {
+        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a[0].x), __uint_as_float(b[0].x), c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a[0].y), __uint_as_float(b[0].y), c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a[0].z), __uint_as_float(b[0].z), c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a[0].w), __uint_as_float(b[0].w), c, 0, 0, 0);
         return c;
     }
     __device__ static __forceinline__ u32x4 pack(const float* f) {
         return u32x4{__float_as_uint(f[0]), __float_as_uint(f[1]), __float_as_uint(f[2]),
                      __float_as_uint(f[3])};
+    }
+};
+
+// E4M3 steps: A is 32 bytes per lane (two units), scaled by 2^(sa - 127)
+// inside the MFMA (E8M0), which undoes the weights' per-layer 2^s; B is the
+// 32 E4M3 activations of the lane (two u32x4 of the chained layout).
+template <>
+struct Prec<kFP8> {
+    static constexpr int E = 32;
+    static constexpr int U = 2;
+    __device__ static __forceinline__ f32x16 mma(const u32x4* a, const u32x4* b, f32x16 c, int sa) {
+        const i32x8 av = {(int)a[0].x, (int)a[0].y, (int)a[0].z, (int)a[0].w,
+                          (int)a[1].x, (int)a[1].y, (int)a[1].z, (int)a[1].w};
+        const i32x8 bv = {(int)b[0].x, (int)b[0].y, (int)b[0].z, (int)b[0].w,
+                          (int)b[1].x, (int)b[1].y, (int)b[1].z, (int)b[1].w};
+        return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bv, c, 0, 0, 0, sa, 0, 127);
     }
 };
 
@@ -115,63 +134,68 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 // The workgroup consumes one logical sequence of chunks: every depth-network
 // chunk, then the shading-network chunks once per sample.  Chunks travel
-// from L2 straight into LDS (global_load_lds, 16 bytes per lane), kRing - 1
-// chunks ahead of use, in a ring of kRing slots.  Each wave copies
+// from L2 straight into LDS (global_load_lds, 16 bytes per lane) one chunk
+// ahead of use, alternating between two LDS arrays.  Every layer holds an
+// even number of chunks (padded with zeros), so chunk j of a layer always
+// sits in slot j & 1 and every read and copy names its array at compile
+// time: reads of one slot then carry a different alias scope from the copy
+// in flight into the other, and need no wait for it.  Each wave copies
 // kChunkFrags / NW fragments of every chunk; advancing to chunk c waits for
-// the wave's own copies of c (later chunks stay in flight) and then
-// barriers, which both publishes c and retires every reader of chunk c-1,
-// whose slot the copy of chunk c + kRing - 1 then reuses.  The copy count per
-// step is constant (the stream index is clamped past its end) so the counter
-// arithmetic holds at the tail.
+// the wave's own copies of c and then barriers, which both publishes c and
+// retires every reader of chunk c - 1, whose slot the copy of c + 1 reuses.
+// The copy count per step is constant (the stream index is clamped past its
+// end) so the counter arithmetic holds at the tail.
 template <int NW>
 struct WeightStream {
     static constexpr int FPW = kChunkFrags / NW;  // fragments each wave copies per chunk
-    static constexpr int AHEAD = kRing - 1;
     static_assert(kChunkFrags % NW == 0, "chunk split");
     const u32x4* dsrc;
     const u32x4* ssrc;
-    u32x4* ring;
+    u32x4* ring0;
+    u32x4* ring1;
     int nd, ns, total;
-    int c;       // chunk being consumed
-    int slot;    // its LDS slot
     int lane, wave;
     int src_k;   // stream index of the next chunk to copy (clamped to total - 1)
     int src_s;   // its position in the shading-network chunks (mod ns)
 
     // Branch-free (selects only), so chunk changes do not split the
     // scheduling region of the MFMA stream around them.
-    __device__ __forceinline__ void issue(int dst_slot) {
+    template <int SLOT>
+    __device__ __forceinline__ void issue() {
         const bool in_d = src_k < nd;
         const u32x4* base = in_d ? dsrc : ssrc;
         const int off = in_d ? src_k : src_s;
         const u32x4* sp = base + (size_t)off * kChunkVec + wave * FPW * 64 + lane;
-        u32x4* dp = ring + dst_slot * kChunkVec + wave * FPW * 64;
-#pragma unroll
-        for (int i = 0; i < FPW; ++i)
-            __builtin_amdgcn_global_load_lds(sp + i * 64, dp + i * 64, 16, 0, 0);
+        u32x4* dp = (SLOT ? ring1 : ring0) + wave * FPW * 64;
+        // a scalar base and lane offset per four copies (the instruction
+        // offset, below 4 KiB, moves both the global and the LDS address by
+        // i KiB), so the copies hold no per-copy address registers
+        sfor<FPW>([&](auto I) {
+            constexpr int grp = CV(I) / 4, sub = CV(I) % 4;
+            __builtin_amdgcn_global_load_lds(sp + grp * 4 * 64, dp + grp * 4 * 64, 16, sub * kFragBytes, 0);
+        });
         const int nk = src_k + 1;
         const bool adv = nk < total;
         src_s = (adv && nk > nd) ? (src_s + 1 == ns ? 0 : src_s + 1) : src_s;
         src_k = adv ? nk : src_k;
     }
     __device__ __forceinline__ void start() {
-        c = -1;
-        slot = kRing - 1;
         src_k = 0;
         src_s = 0;
-#pragma unroll
-        for (int k = 0; k < AHEAD; ++k) issue(k);
+        issue<0>();
     }
+    // Begin the next chunk, which sits in slot PAR.
+    template <int PAR>
     __device__ __forceinline__ void next() {
-        ++c;
-        slot = slot == kRing - 1 ? 0 : slot + 1;
-        wait_vmcnt<FPW * (AHEAD - 1)>();
+        wait_vmcnt<0>();
         lds_barrier();
-        // the slot of chunk c - 1, i.e. the one before c's in ring order
-        issue(slot == 0 ? kRing - 1 : slot - 1);
+        issue<1 - PAR>();
     }
     __device__ __forceinline__ void finish() { wait_vmcnt<0>(); }
-    __device__ __forceinline__ u32x4 frag(int i) const { return ring[slot * kChunkVec + i * 64 + lane]; }
+    template <int PAR>
+    __device__ __forceinline__ u32x4 frag(int i) const {
+        return (PAR ? ring1 : ring0)[i * 64 + lane];
+    }
 };
 
 // ------------------------------------------------------------------ MFMA layers
@@ -194,9 +218,10 @@ __device__ __forceinline__ f32x16 bias_frag(const float* bias, int g) {
 // One accumulator pass: RBP output row blocks x CB column blocks over KS K
 // steps.  BASE is the index of the pass's first fragment within its layer;
 // layers start on chunk boundaries, so chunk changes are known statically.
-template <bool BF16, int CB, int KS, int RBP, int BASE, class WS, class GetB, class Epi>
+template <int PR, int CB, int KS, int RBP, int BASE, class WS, class GetB, class Epi>
 __device__ __forceinline__ void run_pass(WS& st, int g, const float* bias, GetB& getB, Epi&& epi) {
-    using P = Prec<BF16>;
+    using P = Prec<PR>;
+    static_assert(P::U == 1, "heads run single-unit steps");
     constexpr int NF = KS * RBP;   // fragments of the pass, in (K step, row block) order
     constexpr int D = kFragAhead;  // LDS reads issued this many fragments ahead
     f32x16 acc[RBP][CB];
@@ -212,15 +237,16 @@ __device__ __forceinline__ void run_pass(WS& st, int g, const float* bias, GetB&
     sfor<NF + D>([&](auto S) {
         constexpr int s = CV(S);
         if constexpr (s < NF) {
-            constexpr int idx = BASE + s;
-            if constexpr (idx % kChunkFrags == 0) st.next();
-            a[s] = st.frag(idx % kChunkFrags);
+            constexpr int idx = BASE + s;   // BASE counts from an even chunk
+            if constexpr (idx % kChunkFrags == 0) st.template next<(idx / kChunkFrags) & 1>();
+            a[s] = st.template frag<(idx / kChunkFrags) & 1>(idx % kChunkFrags);
         }
         if constexpr (s >= D) {
             constexpr int f = s - D;
             constexpr int k = f / RBP, r = f % RBP;
             sfor<CB>([&](auto C) {
-                acc[r][CV(C)] = P::mma(a[f], getB(std::integral_constant<int, k>{}, C), acc[r][CV(C)]);
+                const u32x4 bk = getB(std::integral_constant<int, k>{}, C);
+                acc[r][CV(C)] = P::mma(&a[f], &bk, acc[r][CV(C)], 127);
             });
         }
         __builtin_amdgcn_sched_barrier(0x6);
@@ -232,10 +258,10 @@ __device__ __forceinline__ void run_pass(WS& st, int g, const float* bias, GetB&
 // [ks0, ks0 + KSPB) of the next layer's B operand.  bf16: round to nearest
 // even, then ReLU on the packed pair as a signed 16-bit max with 0 (rounding
 // preserves the sign, so this equals rounding the ReLU).
-template <bool BF16, int NK, int CB>
+template <int PR, int NK, int CB>
 __device__ __forceinline__ void emit_relu(const f32x16& acc, u32x4 (&out)[NK][CB], int ks0, int cb) {
-    using P = Prec<BF16>;
-    if constexpr (BF16) {
+    using P = Prec<PR>;
+    if constexpr (PR == kBF16) {
         typedef short i16x2 __attribute__((ext_vector_type(2)));
 #pragma unroll
         for (int h = 0; h < P::KSPB; ++h) {
@@ -256,29 +282,56 @@ __device__ __forceinline__ void emit_relu(const f32x16& acc, u32x4 (&out)[NK][CB
     }
 }
 
+// ReLU, clamp to the E4M3 range and round (nearest even) the two 32-row
+// blocks of a pass as K step ks of an fp8 layer's B operand: elements 0-15
+// are block 0's registers, 16-31 block 1's (layout.h chained_row).
+template <int NK, int CB>
+__device__ __forceinline__ void emit_fp8(const f32x16& a0, const f32x16& a1, u32x4 (&out)[NK][CB], int ks,
+                                         int cb) {
+    uint32_t d[8];
+#pragma unroll
+    for (int w = 0; w < 8; ++w) {
+        const f32x16& v = w < 4 ? a0 : a1;
+        const int i = 4 * (w % 4);
+        const float v0 = __builtin_amdgcn_fmed3f(v[i + 0], 0.0f, 448.0f);
+        const float v1 = __builtin_amdgcn_fmed3f(v[i + 1], 0.0f, 448.0f);
+        const float v2 = __builtin_amdgcn_fmed3f(v[i + 2], 0.0f, 448.0f);
+        const float v3 = __builtin_amdgcn_fmed3f(v[i + 3], 0.0f, 448.0f);
+        uint32_t x = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(v0, v1, 0, false);
+        x = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(v2, v3, (int)x, true);
+        d[w] = x;
+    }
+    out[2 * ks][cb] = u32x4{d[0], d[1], d[2], d[3]};
+    out[2 * ks + 1][cb] = u32x4{d[4], d[5], d[6], d[7]};
+}
+
 // Fully connected ReLU layer with 256 outputs (8 row blocks) as one software
 // pipeline over its KS * 8 fragments: passes of kRbPerPass row blocks use
 // alternating accumulator sets, so the bias/ReLU/rounding of pass p can
 // overlap the MFMAs of pass p + 1, and LDS reads run kFragAhead fragments
-// ahead across pass and chunk boundaries.  BF16 is the precision of the
-// output activations; MMA_BF16 that of the layer's own fragments and input
-// (an fp32 layer may feed a bf16 network).
-template <bool BF16, int CB, int KS, bool MMA_BF16 = BF16, class WS, class GetB>
+// ahead across pass and chunk boundaries.  OUT is the precision of the
+// output activations (the next layer's), MP that of the layer's own steps and
+// input; sa is the E8M0 scale of fp8 weights.  getB(k, c) returns the u32x4
+// k of the input (an fp8 step reads two).
+template <int OUT, int CB, int KS, int MP, class WS, class GetB, int NOUT>
 __device__ __forceinline__ void hidden_layer(WS& st, int g, const float* bias, GetB&& getB,
-                                             u32x4 (&out)[8 * Prec<BF16>::KSPB][CB]) {
-    using P = Prec<BF16>;
-    using M = Prec<MMA_BF16>;
+                                             u32x4 (&out)[NOUT][CB], int sa = 127) {
+    using M = Prec<MP>;
+    constexpr int U = M::U;
     constexpr int RBP = kRbPerPass;
-    constexpr int PF = KS * RBP;       // fragments per pass
-    constexpr int NF = 8 * KS;         // fragments of the layer
+    constexpr int PF = KS * RBP;       // steps per pass
+    constexpr int NF = 8 * KS;         // steps of the layer
+    constexpr int SPC = kChunkFrags / U;  // steps per chunk
     constexpr int D = kFragAhead;
+    static_assert(OUT != kFP8 || RBP == 2, "an fp8 K step takes two row blocks");
     f32x16 acc[2][RBP][CB];
-    u32x4 a[D + 1];
+    u32x4 a[D + 1][U];
     sfor<NF + D>([&](auto S) {
         constexpr int s = CV(S);
         if constexpr (s < NF) {
-            if constexpr (s % kChunkFrags == 0) st.next();
-            a[s % (D + 1)] = st.frag(s % kChunkFrags);
+            if constexpr (s % SPC == 0) st.template next<(s / SPC) & 1>();
+#pragma unroll
+            for (int u = 0; u < U; ++u) a[s % (D + 1)][u] = st.template frag<(s / SPC) & 1>((s % SPC) * U + u);
         }
         if constexpr (s >= D) {
             constexpr int f = s - D;
@@ -290,19 +343,27 @@ __device__ __forceinline__ void hidden_layer(WS& st, int g, const float* bias, G
                 });
             }
             sfor<CB>([&](auto C) {
-                acc[p & 1][r][CV(C)] = M::mma(a[f % (D + 1)], getB(std::integral_constant<int, k>{}, C),
-                                              acc[p & 1][r][CV(C)]);
+                u32x4 bk[U];
+                sfor<U>([&](auto V) { bk[CV(V)] = getB(std::integral_constant<int, k * U + CV(V)>{}, C); });
+                acc[p & 1][r][CV(C)] = M::mma(a[f % (D + 1)], bk, acc[p & 1][r][CV(C)], sa);
             });
             if constexpr (w == PF - 1) {
-                sfor<RBP>([&](auto R) {
-                    sfor<CB>([&](auto C) {
-                        emit_relu<BF16>(acc[p & 1][CV(R)][CV(C)], out, (p * RBP + CV(R)) * P::KSPB, CV(C));
+                if constexpr (OUT == kFP8) {
+                    sfor<CB>([&](auto C) { emit_fp8(acc[p & 1][0][CV(C)], acc[p & 1][1][CV(C)], out, p, CV(C)); });
+                } else {
+                    sfor<RBP>([&](auto R) {
+                        sfor<CB>([&](auto C) {
+                            emit_relu<OUT>(acc[p & 1][CV(R)][CV(C)], out, (p * RBP + CV(R)) * Prec<OUT>::KSPB,
+                                           CV(C));
+                        });
                     });
-                });
+                }
             }
         }
         __builtin_amdgcn_sched_barrier(0x6);
     });
+    // a layer of an odd number of chunks is padded to an even one
+    if constexpr (((NF * U + kChunkFrags - 1) / kChunkFrags) & 1) st.template next<1>();
 }
 
 // ------------------------------------------------------------------ selection
@@ -579,30 +640,34 @@ __device__ __forceinline__ void fourier(const float (&v)[3], int g, float* f) {
 
 constexpr int kBiasMax = 7 * 256 + 256 + 7 * 256 + 32;
 
-// BF16: network precision.  CB: 32-ray column blocks per wave.  NW: waves per
-// workgroup.  OCC: waves per SIMD the register budget is sized for (with
+// PR: network precision (layout.h Precision; an fp8 network keeps its first
+// layers and heads in bf16).  CB: 32-ray column blocks per wave.  NW: waves
+// per workgroup.  OCC: waves per SIMD the register budget is sized for (with
 // OCC * 4 > NW several workgroups share a CU).  NCAP: capacity of the top-N
 // list (top-N) or of the sample arrays (CDF).  PLACE: sample placement.
 // DIN: depth-network input (layout.h DepthInput).
-template <bool BF16, int CB, int NW, int OCC, int NCAP, int PLACE, int DIN>
+template <int PR, int CB, int NW, int OCC, int NCAP, int PLACE, int DIN>
 __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(OCC, OCC)))
 render_kernel(const RenderArgs a) {
-    using P = Prec<BF16>;
+    constexpr int FP = PR == kFP8 ? kBF16 : PR;   // first layers, heads, features
+    using P = Prec<FP>;
     constexpr int E = P::E;
-    // first depth layer: K steps of the encoded input (network precision) or
-    // of the folded positions input (always fp32 fragments, 8 K per step)
-    constexpr int KS_D0 = DIN == kDinEncoded ? kDKPad / (2 * E) : kPKPad / (2 * Prec<false>::E);
-    constexpr int KS_H = kHidden / (2 * E);    // 16 | 32
-    constexpr int KS_S0 = kSKPad / (2 * E);    // 4 | 8
-    constexpr int KS_SK = kSkipKPad / (2 * E); // 2 | 4
+    // first depth layer: K steps of the encoded input or of the folded
+    // positions input (always fp32 steps, 8 K each)
+    constexpr int KS_D0 = DIN == kDinEncoded ? kDKPad / (2 * E) : kPKPad / (2 * Prec<kF32>::E);
+    constexpr int KS_H = kHidden / (2 * E);       // heads: 16 | 32
+    constexpr int KS_HID = ksteps(PR, kHidden);   // hidden layers: 16 | 32 | 4
+    constexpr int KS_S0 = kSKPad / (2 * E);       // 4 | 8
+    constexpr int KS_SK = kSkipKPad / (2 * E);    // 2 | 4
 
-    __shared__ u32x4 ring[kRing * kChunkVec];
+    __shared__ u32x4 ring0[kChunkVec];
+    __shared__ u32x4 ring1[kChunkVec];
     __shared__ float bias_s[kBiasMax];
     __shared__ float bins_s[2 * 256];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: lets the stream address one chunk from scalars
     const int g = lane >> 5;
     const int col = lane & 31;
 
@@ -612,7 +677,8 @@ render_kernel(const RenderArgs a) {
     WeightStream<NW> st;
     st.dsrc = reinterpret_cast<const u32x4*>(a.d_frags);
     st.ssrc = reinterpret_cast<const u32x4*>(a.s_frags);
-    st.ring = ring;
+    st.ring0 = ring0;
+    st.ring1 = ring1;
     st.nd = a.n_d_chunks;
     st.ns = a.n_s_chunks;
     // this workgroup's tile and its share of the samples
@@ -649,8 +715,8 @@ render_kernel(const RenderArgs a) {
         v[2] = (ou[2] - a.cz) / a.dmax;
         float f[kDSlots];
         if constexpr (DIN == kDinEncoded) {
-            fourier<5, !BF16>(v, g, f);
-            fourier<2, !BF16>(ray[cb].r, g, f + 30);
+            fourier<5, FP == kF32>(v, g, f);
+            fourier<2, FP == kF32>(ray[cb].r, g, f + 30);
             f[42] = g ? ray[cb].r[0] : v[0];
             f[43] = g ? ray[cb].r[1] : v[1];
             f[44] = g ? ray[cb].r[2] : v[2];
@@ -671,9 +737,9 @@ render_kernel(const RenderArgs a) {
                 q[e] = g ? q9[2 * e + 1] : q9[2 * e];
                 q[4 + e] = (e == 0 && g == 0) ? q9[8] : 0.0f;
             }
-            din[0][cb] = Prec<false>::pack(q);
-            din[1][cb] = Prec<false>::pack(q + 4);
-            fourier<2, !BF16>(ray[cb].r, g, f + 30);
+            din[0][cb] = Prec<kF32>::pack(q);
+            din[1][cb] = Prec<kF32>::pack(q + 4);
+            fourier<2, FP == kF32>(ray[cb].r, g, f + 30);
         }
         // the direction skip of the last shading layer: the same direction
         // encoding plus the identity
@@ -690,25 +756,43 @@ render_kernel(const RenderArgs a) {
     lds_barrier();  // bias_s and bins_s visible
 
     // ---- depth-oracle network
-    // Layers alternate h0 -> h1 -> h0; h0 holds the input of the next layer.
+    // Layers alternate h0 -> h1 -> h0; h0 holds the input of the next layer
+    // (an fp8 layer's input takes the first 2 KS_HID entries).
     u32x4 h0[KS_H][CB], h1[KS_H][CB];
     auto g0 = [&](auto K, auto C) { return h0[CV(K)][CV(C)]; };
     auto g1 = [&](auto K, auto C) { return h1[CV(K)][CV(C)]; };
-    // six 256 -> 256 ReLU layers whose biases start at bias_l0
-    auto hidden6 = [&](const float* bias_l0) {
-        for (int l = 0; l < 3; ++l) {
-            hidden_layer<BF16, CB, KS_H>(st, g, bias_l0 + 256 * (2 * l), g0, h1);
-            hidden_layer<BF16, CB, KS_H>(st, g, bias_l0 + 256 * (2 * l + 1), g1, h0);
+    // six 256 -> 256 ReLU layers whose biases start at bias_l0 and whose fp8
+    // weight scales start at ws; the last one feeds a head in FP
+    auto hidden6 = [&](const float* bias_l0, const int32_t* ws) {
+        if constexpr (PR == kFP8) {
+            for (int l = 0; l < 2; ++l) {
+                hidden_layer<kFP8, CB, KS_HID, kFP8>(st, g, bias_l0 + 256 * (2 * l), g0, h1, ws[2 * l]);
+                hidden_layer<kFP8, CB, KS_HID, kFP8>(st, g, bias_l0 + 256 * (2 * l + 1), g1, h0, ws[2 * l + 1]);
+            }
+            hidden_layer<kFP8, CB, KS_HID, kFP8>(st, g, bias_l0 + 256 * 4, g0, h1, ws[4]);
+            hidden_layer<FP, CB, KS_HID, kFP8>(st, g, bias_l0 + 256 * 5, g1, h0, ws[5]);
+        } else {
+            for (int l = 0; l < 3; ++l) {
+                hidden_layer<PR, CB, KS_HID, PR>(st, g, bias_l0 + 256 * (2 * l), g0, h1);
+                hidden_layer<PR, CB, KS_HID, PR>(st, g, bias_l0 + 256 * (2 * l + 1), g1, h0);
+            }
         }
     };
     {
         auto gin = [&](auto K, auto C) { return din[CV(K)][CV(C)]; };
-        hidden_layer<BF16, CB, KS_D0, DIN == kDinEncoded ? BF16 : false>(st, g, bias_s, gin, h0);
+        hidden_layer<PR, CB, KS_D0, DIN == kDinEncoded ? FP : kF32>(st, g, bias_s, gin, h0);
     }
-    hidden6(bias_s + 256);
+    hidden6(bias_s + 256, a.wscale + 1);
     // Head of the depth network: B / 64 passes of 64 classes (32 * kRbPerPass).
     const int npass = a.B / (32 * kRbPerPass);
     constexpr int PASS_FRAGS = KS_H * kRbPerPass;
+    // A pass spans CPP whole chunks; GP passes make an even number of them
+    // (the head is padded to even chunks, so a missing pass of an odd count
+    // is the padding chunk).
+    static_assert(PASS_FRAGS % kChunkFrags == 0, "a pass spans whole chunks");
+    constexpr int CPP = PASS_FRAGS / kChunkFrags;
+    constexpr int GP = CPP % 2 == 0 ? 1 : 2;
+    static_assert(CPP % 2 == 0 || CPP == 1, "pass grouping");
     auto dump_scores = [&](int p, int R, int C, const f32x16& acc) {
         if (a.out_scores && part == 0 && valid[C]) {
             float* dst = a.out_scores + (size_t)rid[C] * a.B;
@@ -723,14 +807,14 @@ render_kernel(const RenderArgs a) {
     if constexpr (PLACE == kPlaceTopN) {
         TopList<NCAP> top[CB];
         sfor<CB>([&](auto C) { top[CV(C)].init(); });
-        // PPC passes share one chunk, so the loop steps a chunk at a time.
-        constexpr int PPC = PASS_FRAGS >= kChunkFrags ? 1 : kChunkFrags / PASS_FRAGS;
-        for (int p0 = 0; p0 < npass; p0 += PPC) {
-            sfor<PPC>([&](auto Q) {
+        for (int p0 = 0; p0 < npass; p0 += GP) {
+            sfor<GP>([&](auto Q) {
                 constexpr int q = CV(Q);
                 const int p = p0 + q;
-                if (p < npass) {
-                    run_pass<BF16, CB, KS_H, kRbPerPass, q * PASS_FRAGS>(
+                if (p >= npass) {
+                    if constexpr (CPP == 1) st.template next<q & 1>();   // padding chunk
+                } else {
+                    run_pass<FP, CB, KS_H, kRbPerPass, q * PASS_FRAGS>(
                         st, g, bias_s + 7 * 256 + 32 * kRbPerPass * p, g0, [&](auto R, auto C, const f32x16& acc) {
                             const int rowb = 32 * kRbPerPass * p + 32 * CV(R) + 4 * g;
 #pragma unroll
@@ -753,13 +837,14 @@ render_kernel(const RenderArgs a) {
         sfor<NPM>([&](auto PI) {
             constexpr int p = CV(PI);
             if (p < npass) {
-                run_pass<BF16, CB, KS_H, kRbPerPass, p * PASS_FRAGS>(
+                run_pass<FP, CB, KS_H, kRbPerPass, p * PASS_FRAGS>(
                     st, g, bias_s + 7 * 256 + 32 * kRbPerPass * p, g0, [&](auto R, auto C, const f32x16& acc) {
 #pragma unroll
                         for (int i = 0; i < 16; ++i) vals[CV(C)][p][CV(R)][i] = 1.0f / (1.0f + expf(-acc[i]));
                         dump_scores(p, CV(R), CV(C), acc);
                     });
             } else {
+                if constexpr (CPP == 1 && (p & 1)) st.template next<1>();   // padding chunk
                 sfor<CB>([&](auto C) {
 #pragma unroll
                     for (int R = 0; R < kRbPerPass; ++R)
@@ -804,7 +889,7 @@ render_kernel(const RenderArgs a) {
             for (int c = 0; c < 3; ++c) x[c] = ray[cb].o[c] + tk[cb] * ray[cb].r[c];
             warp(a, x, w);
             float f[kSSlots];
-            fourier<5, !BF16>(w, g, f);
+            fourier<5, FP == kF32>(w, g, f);
             f[30] = g ? w[2] : w[0];
             f[31] = g ? 0.0f : w[1];
 #pragma unroll
@@ -812,14 +897,14 @@ render_kernel(const RenderArgs a) {
         }
         {
             auto gs = [&](auto K, auto C) { return sin_[CV(K)][CV(C)]; };
-            hidden_layer<BF16, CB, KS_S0>(st, g, bias_s + s_bias, gs, h0);
+            hidden_layer<PR, CB, KS_S0, FP>(st, g, bias_s + s_bias, gs, h0);
         }
-        hidden6(bias_s + s_bias + 256);
+        hidden6(bias_s + s_bias + 256, a.wscale + 9);
         auto gh = [&](auto K, auto C) {
             if constexpr (CV(K) < KS_H) return h0[CV(K)][CV(C)];
             else return skip[CV(K) - KS_H][CV(C)];
         };
-        run_pass<BF16, CB, KS_H + KS_SK, 1, 0>(
+        run_pass<FP, CB, KS_H + KS_SK, 1, 0>(
             st, g, bias_s + s_bias + 7 * 256, gh, [&](auto R, auto C, const f32x16& acc) {
                 constexpr int cb = CV(C);
                 // lanes of group 0 hold rows 0..3 = (r, g, b, sigma) in registers 0..3
@@ -836,6 +921,8 @@ render_kernel(const RenderArgs a) {
                 Dp[cb] += wgt * tk[cb];
                 T[cb] *= expf(-tau);
             });
+        // the shading head is padded to an even number of chunks
+        if constexpr ((((KS_H + KS_SK) + kChunkFrags - 1) / kChunkFrags) & 1) st.template next<1>();
     }
     st.finish();  // no copy into LDS may outlive the workgroup
 
@@ -874,22 +961,22 @@ render_kernel(const RenderArgs a) {
 }
 
 // One render variant; ncap selects the sample capacity.
-template <bool B16, int CB, int NW, int OCC, int PL, int DIN>
+template <int PR, int CB, int NW, int OCC, int PL, int DIN>
 hipError_t launch_variant(int ncap, const RenderArgs& a, dim3 grid, hipStream_t stream) {
     if (ncap == 4)
-        hipLaunchKernelGGL((render_kernel<B16, CB, NW, OCC, 4, PL, DIN>), grid, dim3(64 * NW), 0, stream, a);
+        hipLaunchKernelGGL((render_kernel<PR, CB, NW, OCC, 4, PL, DIN>), grid, dim3(64 * NW), 0, stream, a);
     else if (ncap == 8)
-        hipLaunchKernelGGL((render_kernel<B16, CB, NW, OCC, 8, PL, DIN>), grid, dim3(64 * NW), 0, stream, a);
+        hipLaunchKernelGGL((render_kernel<PR, CB, NW, OCC, 8, PL, DIN>), grid, dim3(64 * NW), 0, stream, a);
     else
-        hipLaunchKernelGGL((render_kernel<B16, CB, NW, OCC, 16, PL, DIN>), grid, dim3(64 * NW), 0, stream, a);
+        hipLaunchKernelGGL((render_kernel<PR, CB, NW, OCC, 16, PL, DIN>), grid, dim3(64 * NW), 0, stream, a);
     return hipGetLastError();
 }
 
 // Both depth inputs of one precision and placement.
-template <bool B16, int CB, int NW, int OCC, int PL>
+template <int PR, int CB, int NW, int OCC, int PL>
 hipError_t launch_placement(int ncap, int din, const RenderArgs& a, dim3 grid, hipStream_t stream) {
-    return din == kDinPositions ? launch_variant<B16, CB, NW, OCC, PL, kDinPositions>(ncap, a, grid, stream)
-                                : launch_variant<B16, CB, NW, OCC, PL, kDinEncoded>(ncap, a, grid, stream);
+    return din == kDinPositions ? launch_variant<PR, CB, NW, OCC, PL, kDinPositions>(ncap, a, grid, stream)
+                                : launch_variant<PR, CB, NW, OCC, PL, kDinEncoded>(ncap, a, grid, stream);
 }
 
 }  // namespace
