@@ -23,7 +23,7 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}   # MI355X dense peaks
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3, "fp8": 5000.0}   # MI355X dense peaks
 HBM_PEAK_GBS = 8000.0
 
 # HBM bytes per render dispatch of the default workload, from two
@@ -61,6 +61,21 @@ def algorithmic_flop_per_ray(N: int, n_bins: int, d_in: int = 90) -> int:
     d = d_in * 256 + 6 * 256 * 256 + 256 * n_bins
     s = 63 * 256 + 6 * 256 * 256 + (256 + 27) * 4
     return 2 * (d + N * s)
+
+
+def fp8_flop_per_ray(N: int) -> int:
+    """The part of the algorithmic work the mixed fp8 network runs in fp8:
+    the six 256 -> 256 hidden layers of both networks."""
+    return 2 * 6 * 256 * 256 * (1 + N)
+
+
+def mixed_peak(N: int, n_bins: int, d_in: int) -> float:
+    """Peak of the mixed fp8 network: the time its work takes at the fp8 and
+    bf16 dense peaks, each part at its own."""
+    tot = algorithmic_flop_per_ray(N, n_bins, d_in)
+    f8 = fp8_flop_per_ray(N)
+    t = f8 / MFMA_PEAK_TFLOPS["fp8"] + (tot - f8) / MFMA_PEAK_TFLOPS["bf16"]
+    return tot / t
 
 
 def padded_flop_per_ray(N: int, n_bins: int, d_in: int = 90) -> int:
@@ -134,7 +149,7 @@ def main():
     weights = inputs.make_weights(wl.n_bins, 0, wl.depth_input)
     poses = wl.poses()
     P = len(poses)
-    prec = b.BF16 if wl.precision == "bf16" else b.FP32
+    prec = {"bf16": b.BF16, "fp32": b.FP32, "fp8": b.FP8}[wl.precision]
     sel = {"topn": b.SELECT_TOPN, "topn_softmax": b.SELECT_TOPN_SOFTMAX, "cdf": b.SELECT_CDF}[wl.select]
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
@@ -169,7 +184,7 @@ def main():
     d_in = depth_in_folded(wl.depth_input)
     flop_launch = algorithmic_flop_per_ray(wl.N, wl.n_bins, d_in) * rays
     achieved = flop_launch / (avg_kern_ms * 1e-3) / 1e12
-    peak = MFMA_PEAK_TFLOPS[wl.precision]
+    peak = (mixed_peak(wl.N, wl.n_bins, d_in) if wl.precision == "fp8" else MFMA_PEAK_TFLOPS[wl.precision])
     paper_mrays = 400 * 400 / 22e-3 / 1e6   # 22 ms per 400x400 frame, N = 4
     traffic = None
     kib = args.traffic_kib
@@ -200,6 +215,8 @@ def main():
                    "padded_mflop_per_ray": round(padded_flop_per_ray(wl.N, wl.n_bins, d_in) / 1e6, 4)},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(achieved / peak, 4),
+                     **({"peak_note": "fp8 hidden layers at 5000, bf16 first layers and heads at 2500, "
+                                      "combined by their share of the work"} if wl.precision == "fp8" else {}),
                      "traffic": traffic,
                      "kernel": f"render_kernel<{wl.precision}>", "kernel_ms": round(avg_kern_ms, 4)},
     }

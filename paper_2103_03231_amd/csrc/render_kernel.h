@@ -350,6 +350,25 @@ __device__ __forceinline__ void hidden_layer(WS& st, int g, const float* bias, G
             if constexpr (w == PF - 1) {
                 if constexpr (OUT == kFP8) {
                     sfor<CB>([&](auto C) { emit_fp8(acc[p & 1][0][CV(C)], acc[p & 1][1][CV(C)], out, p, CV(C)); });
+                    // Pin the pass's outputs here: layers outside a loop
+                    // could otherwise have their pure MFMA chains sunk past
+                    // the later chunk barriers to the blocks that use them,
+                    // holding every fragment of those chunks in registers.
+                    sfor<CB>([&](auto C) {
+                        const u32x4 o0 = out[2 * p][CV(C)], o1 = out[2 * p + 1][CV(C)];
+                        asm volatile("" ::"v"(o0), "v"(o1));
+                    });
+                } else if constexpr (MP == kFP8) {
+                    sfor<RBP>([&](auto R) {
+                        sfor<CB>([&](auto C) {
+                            emit_relu<OUT>(acc[p & 1][CV(R)][CV(C)], out, (p * RBP + CV(R)) * Prec<OUT>::KSPB,
+                                           CV(C));
+                            sfor<Prec<OUT>::KSPB>([&](auto H) {
+                                const u32x4 o = out[(p * RBP + CV(R)) * Prec<OUT>::KSPB + CV(H)][CV(C)];
+                                asm volatile("" ::"v"(o));
+                            });
+                        });
+                    });
                 } else {
                     sfor<RBP>([&](auto R) {
                         sfor<CB>([&](auto C) {

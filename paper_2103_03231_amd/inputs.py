@@ -178,7 +178,7 @@ class Workload:
     N: int
     n_bins: int = 128
     fov_deg: float = 60.0
-    precision: str = "bf16"          # 'fp32' or 'bf16'
+    precision: str = "bf16"          # 'fp32', 'bf16' or 'fp8' (the mixed network)
     select: str = "topn"              # 'topn', 'topn_softmax' or 'cdf'
     depth_input: str = "encoded"      # 'encoded' (90 inputs) or 'positions' (6 + 3 B)
     want_depth: bool = False
@@ -210,6 +210,7 @@ WORKLOADS = {
                                      select="cdf", want_depth=True),
     "frame400_n4_positions_bf16": Workload("frame400_n4_positions_bf16", 400, 400, (0, 1, 2, 3, 4), 4,
                                            depth_input="positions"),
+    "frame400_n4_fp8": Workload("frame400_n4_fp8", 400, 400, (0, 1, 2, 3, 4), 4, precision="fp8"),
     "frame800_n8_depth_bf16": Workload("frame800_n8_depth_bf16", 800, 800, (0, 1, 2, 3, 4), 8,
                                        want_depth=True),
     "hd1080_n4_softmax_bf16": Workload("hd1080_n4_softmax_bf16", 1080, 1920, tuple(range(10)), 4,

@@ -18,8 +18,12 @@ from paper_2103_03231_amd import inputs
 
 pytestmark = pytest.mark.gpu
 
-TOL = {"fp32": 1e-4, "bf16": 2e-2}
-PREC = {"fp32": b.FP32, "bf16": b.BF16}
+# RGB bars: the contract's fp32 and bf16 tolerances; the fp8 network's bar
+# is a distribution (FP8_BAR, see check_fp8).
+TOL = {"fp32": 1e-4, "bf16": 2e-2, "fp8": 2e-2}
+PREC = {"fp32": b.FP32, "bf16": b.BF16, "fp8": b.FP8}
+# share of rays whose selection may differ from the oracle's (near ties)
+FLIPS = {"fp32": 0.0, "bf16": 0.03, "fp8": 0.05}
 
 
 def log(*a):
@@ -48,16 +52,17 @@ def check_against_oracle(g, w, poses, H, W, N, precision, n_bins=128, fov=60.0, 
     gb = g["bins"].reshape(-1, N)
     rgb = g["rgb"].reshape(-1, 3)
     depth = g["depth"].reshape(-1)
-    scores = g["scores"].reshape(-1, n_bins)
+    scores = g["scores"].reshape(-1, n_bins) if "scores" in g else None
     if subset is not None:
-        gb, rgb, depth, scores = gb[subset], rgb[subset], depth[subset], scores[subset]
+        gb, rgb, depth = gb[subset], rgb[subset], depth[subset]
+        scores = None if scores is None else scores[subset]
     ora = O.render(w, poses, H, W, N, n_bins=n_bins, fov_x_deg=fov, precision=precision,
                    forced_bins=gb, ray_subset=subset, depth_input=depth_input)
     natural = O.topn(ora["logits"].astype(np.float32), N)
     flips = np.any(natural != gb, axis=1)
     err = np.abs(rgb - ora["rgb"]).max()
     derr = np.abs(depth - ora["depth"]).max()
-    serr = np.abs(scores - ora["logits"]).max()
+    serr = np.nan if scores is None else np.abs(scores - ora["logits"]).max()
     log(f"[{label}] rays={len(gb)} flips={flips.sum()} rgb_maxabs={err:.3e} depth_maxabs={derr:.3e} "
         f"score_maxabs={serr:.3e}")
     assert np.all(np.isfinite(rgb)) and np.all((rgb >= 0) & (rgb <= 1))
@@ -454,5 +459,117 @@ def test_positions_variants(precision, N, B, H, W, P, select):
         assert cerr <= CDF_COORD_TOL and err <= TOL[precision]
     else:
         check_against_oracle(g, w, poses, H, W, N, precision, n_bins=B, label=label,
-                             max_flip_frac=0.0 if precision == "fp32" else 0.03, depth_input="positions")
+                             max_flip_frac=FLIPS[precision], depth_input="positions")
     r.close()
+
+
+# ------------------------------------------------------------------ the mixed fp8 network
+
+# The fp8 network's rounding is discontinuous at the scale that matters: an
+# accumulation-order difference (fp32 MFMA vs the oracle's fp64) that
+# straddles an E4M3 rounding boundary moves that activation by a whole E4M3
+# step (1/16 to 1/8 of it), which shifts every pre-activation of the next
+# layer by about W x that step and flips further roundings there.  Most rays
+# agree to fp32 noise; a few per cent cascade into another, equally valid,
+# fp8 evaluation.  The bar is therefore a distribution: the median ray within
+# 1e-3 (with 16 samples per ray about half the rays hold one diverged
+# sample; with 4, the median ray agrees to 1e-5), the 99th percentile within
+# the bf16 bar, every ray within 5e-2, or 0.25 with inverse-CDF slices, whose
+# widths (up to ~5 against class widths <= 0.2) multiply the density
+# difference of a diverged sample.
+FP8_BAR = {"p50": 1e-3, "p99": 2e-2, "max_topn": 5e-2, "max_cdf": 0.25}
+
+
+def check_fp8(err, label, cdf=False):
+    p50, p99 = np.percentile(err, 50), np.percentile(err, 99)
+    log(f"[{label}] rgb p50={p50:.2e} p99={p99:.2e} max={err.max():.2e}")
+    assert p50 <= FP8_BAR["p50"], p50
+    assert p99 <= FP8_BAR["p99"], p99
+    assert err.max() <= FP8_BAR["max_cdf" if cdf else "max_topn"], err.max()
+
+
+@pytest.mark.parametrize("N,B,H,W,P,select,din", [
+    (4, 128, 32, 32, 1, "topn", "encoded"),
+    (1, 64, 17, 23, 1, "topn", "encoded"),
+    (8, 256, 16, 24, 1, "topn", "encoded"),
+    (16, 192, 12, 20, 2, "topn", "encoded"),
+    (4, 128, 24, 40, 1, "topn", "positions"),
+    (4, 128, 24, 40, 1, "cdf", "encoded"),
+])
+def test_fp8_variants(N, B, H, W, P, select, din):
+    """fp8 path against the oracle's fp8 network (same rounding points: E4M3
+    weights with the same per-layer scales, E4M3 activations clamped to 448,
+    bf16 first layers and heads), teacher-forced on the GPU's selection or
+    samples, to FP8_BAR; up to 5 % of rays may select differently."""
+    sel = b.SELECT_CDF if select == "cdf" else b.SELECT_TOPN
+    r, w = renderer("fp8", n_bins=B, n_max=max(N, 4), select=sel, seed=5, depth_input=din)
+    poses = inputs.make_poses(list(range(30, 30 + P)))
+    g = gpu_render(r, poses, H, W, N)
+    label = f"fp8 {select} {din} N={N} B={B} {P}x{H}x{W}"
+    if select == "cdf":
+        samp = g["samples"].reshape(-1, N, 2)
+        t_ref, _, _ = O.cdf_samples(g["scores"].reshape(-1, B), N, 0.1, 10.0)
+        cerr = np.abs(_log_coord(samp[..., 0]) - _log_coord(t_ref)).max()
+        assert cerr <= CDF_COORD_TOL, cerr
+        ora = O.render(w, poses, H, W, N, n_bins=B, precision="fp8", select="cdf",
+                       forced_samples=(samp[..., 0], samp[..., 1]), depth_input=din)
+    else:
+        gb = g["bins"].reshape(-1, N)
+        ora = O.render(w, poses, H, W, N, n_bins=B, precision="fp8", forced_bins=gb, depth_input=din)
+        flips = np.any(O.topn(ora["logits"].astype(np.float32), N) != gb, axis=1)
+        log(f"[{label}] flips={flips.sum()} of {len(gb)}")
+        assert flips.mean() <= FLIPS["fp8"]
+    check_fp8(np.abs(g["rgb"].reshape(-1, 3) - ora["rgb"]).max(1), label, cdf=select == "cdf")
+    r.close()
+
+
+def test_fp8_frame400_sampled():
+    r, w = renderer("fp8")
+    poses = inputs.make_poses(range(5))
+    out = r.alloc(5, 400, 400, 4, depth=True)
+    out["bins"] = torch.empty((5, 400, 400, 4), dtype=torch.int32, device="cuda")
+    r.render_into(poses, 400, 400, 4, out, debug=True)
+    torch.cuda.synchronize()
+    g = {k: v.cpu().numpy() for k, v in out.items()}
+    subset = np.unique(np.random.default_rng(4).integers(0, 5 * 400 * 400, 2000))
+    gb = g["bins"].reshape(-1, 4)[subset]
+    ora = O.render(w, poses, 400, 400, 4, precision="fp8", forced_bins=gb, ray_subset=subset)
+    flips = np.any(O.topn(ora["logits"].astype(np.float32), 4) != gb, axis=1)
+    assert flips.mean() <= FLIPS["fp8"]
+    check_fp8(np.abs(g["rgb"].reshape(-1, 3)[subset] - ora["rgb"]).max(1), "fp8 5x400x400")
+    r.close()
+
+
+def test_fp8_tolerance_study():
+    """How far the fp8 network moves the image from the bf16 and fp64 ones
+    (He-initialised weights, 2000 rays of the 5 x 400 x 400 frame, each
+    network with its own selection).  Logged for the record; the asserted
+    bounds only guard against a regression."""
+    w = inputs.make_weights(128, 0)
+    poses = inputs.make_poses(range(5))
+    res = {}
+    for prec in ("fp8", "bf16"):
+        r = b.Renderer(b.Config(precision=PREC[prec]), w)
+        out = r.alloc(5, 400, 400, 4, depth=True)
+        out["bins"] = torch.empty((5, 400, 400, 4), dtype=torch.int32, device="cuda")
+        r.render_into(poses, 400, 400, 4, out, debug=True)
+        torch.cuda.synchronize()
+        res[prec] = {k: v.cpu().numpy() for k, v in out.items()}
+        r.close()
+    subset = np.unique(np.random.default_rng(6).integers(0, 5 * 400 * 400, 2000))
+    o64 = O.render(w, poses, 400, 400, 4, ray_subset=subset)
+    ob16 = O.render(w, poses, 400, 400, 4, precision="bf16", ray_subset=subset)
+    rgb8 = res["fp8"]["rgb"].reshape(-1, 3)[subset]
+    rgb16 = res["bf16"]["rgb"].reshape(-1, 3)[subset]
+    bins8 = res["fp8"]["bins"].reshape(-1, 4)[subset]
+    psnr = lambda a, b_: 10 * np.log10(1.0 / np.mean((a - b_) ** 2))
+    stats = {
+        "fp8_vs_fp64_psnr": psnr(rgb8, o64["rgb"]), "bf16_vs_fp64_psnr": psnr(rgb16, o64["rgb"]),
+        "fp8_vs_bf16oracle_psnr": psnr(rgb8, ob16["rgb"]),
+        "fp8_vs_fp64_mean_abs": np.abs(rgb8 - o64["rgb"]).mean(), "fp8_vs_fp64_max_abs": np.abs(rgb8 - o64["rgb"]).max(),
+        "bf16_vs_fp64_mean_abs": np.abs(rgb16 - o64["rgb"]).mean(),
+        "fp8_selection_differs_from_fp64": np.mean(np.any(bins8 != o64["bins"], axis=1)),
+        "bf16_selection_differs_from_fp64": np.mean(np.any(res["bf16"]["bins"].reshape(-1, 4)[subset] != o64["bins"], axis=1)),
+    }
+    log("[fp8 study] " + " ".join(f"{k}={v:.4g}" for k, v in stats.items()))
+    assert stats["fp8_vs_fp64_psnr"] > 25.0 and stats["bf16_vs_fp64_psnr"] > stats["fp8_vs_fp64_psnr"]
