@@ -200,6 +200,28 @@ int donerf_debug_topn(donerf_t* h, const float* scores, int32_t rays, int32_t N,
                       int32_t* out_idx);
 
 /*
+ * Training targets of the depth oracle (Sec. 5.1) for P depth maps, on the
+ * handle's depth classes and stream:
+ *   Eq. 6  C(z) = 1 for the class z with b_z <= d < b_{z+1} of the pixel's
+ *          first-surface depth d (no class where d is outside [d_min, d_max)
+ *          or not finite),
+ *   Eq. 7  C^(z) = max over the K x K window of C_{x+i,y+j}(z) minus
+ *          sqrt(i^2 + j^2) / (sqrt(2) floor(K/2)) (neighbours outside the
+ *          image left out; K = 1 keeps C),
+ *   Eq. 8  C`(z) = min(sum_{|i| <= floor(Z/2)} C^(z + i) (floor(Z/2) + 1 - |i|)
+ *          / (floor(Z/2) + 1), 1) (classes outside [0, B) left out).
+ *   depth  device, P x H x W fp32: the distance from the camera to the first
+ *          surface along each pixel's ray (Eq. 1's d), row-major
+ *   K, Z   window sizes, 1..15 (the paper uses 5 and 9)
+ *   out    device, P x H x W x B fp32, caller-owned; B = cfg.n_bins
+ * Enqueued on the handle's stream; no allocation.
+ * Errors: E_INVALID_ARG (NULL, P, H, W < 1, K or Z out of range, too many
+ * pixels), E_HIP.
+ */
+int donerf_targets(donerf_t* h, const float* depth, int32_t P, int32_t H, int32_t W, int32_t K, int32_t Z,
+                   float* out);
+
+/*
  * Copy the handle's depth-class table to host memory: bounds (B + 1 values,
  * may be NULL), centres (B), widths (B).  Bounds b_k = d_min + (d_max - d_min
  * + 1)^(k/B) - 1 (the inverse of Eq. 3 on a uniform grid), centres at

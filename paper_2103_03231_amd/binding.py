@@ -37,8 +37,8 @@ MAX_SAMPLES = 16
 
 # Every function include/donerf.h declares.
 EXPORTS = ("donerf_weight_count", "donerf_create", "donerf_destroy", "donerf_set_stream",
-           "donerf_render", "donerf_render_debug", "donerf_debug_topn", "donerf_debug_bins",
-           "donerf_status_str", "donerf_last_error")
+           "donerf_render", "donerf_render_debug", "donerf_targets", "donerf_debug_topn",
+           "donerf_debug_bins", "donerf_status_str", "donerf_last_error")
 
 
 class DonerfLibraryMissing(RuntimeError):
@@ -104,6 +104,8 @@ def lib():
         L.donerf_render.restype = ctypes.c_int
         L.donerf_render_debug.argtypes = [vp, fp, i32, i32, i32, i32, vp, vp, vp, vp, vp]
         L.donerf_render_debug.restype = ctypes.c_int
+        L.donerf_targets.argtypes = [vp, vp, i32, i32, i32, i32, i32, vp]
+        L.donerf_targets.restype = ctypes.c_int
         L.donerf_debug_topn.argtypes = [vp, vp, i32, i32, vp]
         L.donerf_debug_topn.restype = ctypes.c_int
         L.donerf_debug_bins.argtypes = [vp, fp, fp, fp]
@@ -168,6 +170,10 @@ def donerf_render_debug(h, poses, P, H, W, N, out_rgb_ptr, out_depth_ptr=None,
                                      out_bins_ptr, out_scores_ptr, out_samples_ptr))
 
 
+def donerf_targets(h, depth_ptr, P, H, W, K, Z, out_ptr) -> None:
+    _check(lib().donerf_targets(h, depth_ptr, P, H, W, K, Z, out_ptr))
+
+
 def donerf_debug_topn(h, scores_ptr, rays, N, out_idx_ptr) -> None:
     _check(lib().donerf_debug_topn(h, scores_ptr, rays, N, out_idx_ptr))
 
@@ -201,6 +207,16 @@ class Renderer:
             self.close()
         except Exception:
             pass
+
+    def targets(self, depth, K, Z):
+        """Depth-oracle targets of device depth maps (P, H, W) fp32 -> (P, H, W, B)."""
+        t = self.torch
+        if depth.dtype != t.float32 or not depth.is_cuda or not depth.is_contiguous() or depth.dim() != 3:
+            raise ValueError("depth must be a contiguous (P, H, W) float32 CUDA tensor")
+        P, H, W = depth.shape
+        out = t.empty((P, H, W, self.cfg.n_bins), dtype=t.float32, device=depth.device)
+        donerf_targets(self.h, depth.data_ptr(), P, H, W, K, Z, out.data_ptr())
+        return out
 
     def alloc(self, P, H, W, N, depth=False, debug=False):
         t = self.torch

@@ -22,7 +22,7 @@ struct donerf_handle {
     hipStream_t stream;
     void* d_frags;       // device: depth stream then shading stream
     float* bias;         // device
-    float* bins;         // device: centres[B], widths[B]
+    float* bins;         // device: centres[B], widths[B], bounds[B + 1]
     int n_d_chunks, n_s_chunks, bias_len;
     int n_cu;            // compute units: workgroups of one full round
     float* partial;      // device: split-tail parts, n_cu * 256 rays * 5 floats
@@ -426,9 +426,10 @@ int donerf_create(const donerf_cfg* cfg, const float* weights, size_t n_weights,
     h->h_bounds = bounds;
     h->h_centres = centres;
     h->h_widths = widths;
-    std::vector<float> bins(2 * B);
+    std::vector<float> bins(3 * B + 1);
     std::memcpy(bins.data(), h->h_centres.data(), sizeof(float) * B);
     std::memcpy(bins.data() + B, h->h_widths.data(), sizeof(float) * B);
+    std::memcpy(bins.data() + 2 * B, h->h_bounds.data(), sizeof(float) * (B + 1));
 
     hipError_t e;
     if ((e = hipDeviceGetAttribute(&h->n_cu, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess ||
@@ -489,6 +490,21 @@ int donerf_debug_topn(donerf_t* h, const float* scores, int32_t rays, int32_t N,
     if (N < 1 || N > h->cfg.n_max || N > h->cfg.n_bins) return fail(DONERF_E_INVALID_ARG, "N out of range");
     hipError_t e = launch_topn(h->prec != kF32, ncap_for(N), scores, rays, N, h->cfg.n_bins, out_idx, h->stream);
     if (e != hipSuccess) return hip_fail(e, "topn launch");
+    return DONERF_OK;
+}
+
+int donerf_targets(donerf_t* h, const float* depth, int32_t P, int32_t H, int32_t W, int32_t K, int32_t Z,
+                   float* out) {
+    g_err.clear();
+    if (!h) return fail(DONERF_E_INVALID_ARG, "handle is NULL");
+    if (!depth || !out) return fail(DONERF_E_INVALID_ARG, "NULL buffer");
+    if (P < 1 || H < 1 || W < 1) return fail(DONERF_E_INVALID_ARG, "P, H and W must be >= 1");
+    if (K < 1 || K > kTgtMaxK || Z < 1 || Z > kTgtMaxK)
+        return fail(DONERF_E_INVALID_ARG, "K and Z must lie in [1, 15]");
+    if ((int64_t)P * H * ((W + 63) / 64) >= ((int64_t)1 << 31)) return fail(DONERF_E_INVALID_ARG, "too many pixels");
+    const int B = h->cfg.n_bins;
+    hipError_t e = launch_targets(depth, P, H, W, h->bins + 2 * B, B, K, Z, out, h->stream);
+    if (e != hipSuccess) return hip_fail(e, "targets launch");
     return DONERF_OK;
 }
 

@@ -82,4 +82,11 @@ hipError_t launch_softmax_rows(float* scores, uint32_t rows, int B, hipStream_t 
 hipError_t launch_topn(bool bf16_layout, int ncap, const float* scores, int32_t rays,
                        int32_t N, int32_t B, int32_t* out_idx, hipStream_t stream);
 
+// Training targets (targets.hip): P depth maps of H x W, class bounds
+// bounds[0..B], window sizes K and Z (1..kTgtMaxK), out P x H x W x B.
+constexpr int kMaxBins = 256;
+constexpr int kTgtMaxK = 15;
+hipError_t launch_targets(const float* depth, int P, int H, int W, const float* bounds, int B, int K, int Z,
+                          float* out, hipStream_t stream);
+
 }  // namespace donerf

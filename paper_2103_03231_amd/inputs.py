@@ -141,6 +141,36 @@ def make_poses(seeds, radius: float = 1.5) -> np.ndarray:
     return np.stack([make_pose(s, radius) for s in seeds])
 
 
+def make_depth_maps(P: int, H: int, W: int, seed: int, near: float = 0.1, far: float = 10.0,
+                    shapes: int = 12) -> np.ndarray:
+    """Seeded synthetic first-surface depth maps (P, H, W) fp32 with the
+    structure of rendered scenes: a background without surface (+inf), and
+    front-most of `shapes` discs and rectangles, each a tilted plane patch
+    whose depth is log-uniform in [near, far] (z-buffered, so objects occlude
+    and depth jumps at their edges).  A few pixels fall outside [near, far)
+    or are NaN (invalid samples)."""
+    rng = SplitMix64(0xDE97 + 104729 * seed)
+    out = np.full((P, H, W), np.inf, dtype=np.float64)
+    yy, xx = np.mgrid[0:H, 0:W].astype(np.float64)
+    for p in range(P):
+        for _ in range(shapes):
+            u = rng.uniform(8)
+            cx, cy = u[0] * W, u[1] * H
+            rad = (0.08 + 0.3 * u[2]) * min(H, W)
+            d0 = near * (far / near) ** u[3]
+            gx, gy = (u[4] - 0.5) * 4.0 * d0 / W, (u[5] - 0.5) * 4.0 * d0 / H
+            if u[6] < 0.5:
+                inside = (xx - cx) ** 2 + (yy - cy) ** 2 <= rad * rad
+            else:
+                inside = (np.abs(xx - cx) <= rad) & (np.abs(yy - cy) <= rad * (0.5 + u[7]))
+            d = np.maximum(d0 + gx * (xx - cx) + gy * (yy - cy), 0.5 * near)
+            out[p] = np.where(inside, np.minimum(out[p], d), out[p])
+        u = rng.uniform(2 * H * W).reshape(2, H, W)
+        out[p][u[0] < 0.002] = np.nan
+        out[p][u[1] < 0.002] = far * 1.5
+    return out.astype(np.float32)
+
+
 def random_logits(rays: int, n_bins: int, seed: int, mode: str = "normal") -> np.ndarray:
     """Seeded logit rows for selection tests.
 

@@ -91,6 +91,7 @@ def test_calls_on_null_handle():
     for fn in (lambda: b.donerf_render(None, poses, 1, 4, 4, 4, 1),
                lambda: b.donerf_render_debug(None, poses, 1, 4, 4, 4, 1),
                lambda: b.donerf_debug_topn(None, 1, 4, 4, 1),
+               lambda: b.donerf_targets(None, 1, 1, 4, 4, 5, 5, 1),
                lambda: b.donerf_debug_bins(None, 128),
                lambda: b.donerf_set_stream(None, 0)):
         with pytest.raises(b.DonerfError) as e:
