@@ -26,22 +26,33 @@ sys.path.insert(0, ROOT)
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3, "fp8": 5000.0}   # MI355X dense peaks
 HBM_PEAK_GBS = 8000.0
 
-# HBM bytes per render dispatch of the default workload, from two
-# rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE; profiles/
-# render_kernel_frame400_n4_bf16_traffic.md) scaled by the same counters on a
-# plain 256 MiB copy (FETCH_SIZE reads half the bytes moved: x2; WRITE_SIZE
-# exact: x1).  Valid only for the kernel sources they were taken on.
-MEASURED_TRAFFIC = {"sources_sha256_16": "94017e4f7e55b4c5", "workload": "frame400_n4_bf16",
-                    "fetch_kib": 7338.9 * 2, "write_kib": 11760.0}
-# the sources the bf16 top-N render kernel is built from
-KERNEL_SOURCES = ("paper_2103_03231_amd/csrc/render_kernel.h", "paper_2103_03231_amd/csrc/render_bf16_topn.hip",
-                  "paper_2103_03231_amd/csrc/layout.h", "paper_2103_03231_amd/csrc/internal.h")
+# HBM KiB per dispatch from two rocprofv3 --pmc runs (FETCH_SIZE, then
+# WRITE_SIZE; profiles/*_traffic.md) scaled by the same counters on a plain
+# 256 MiB copy (FETCH_SIZE reads half the bytes moved: x2; WRITE_SIZE exact:
+# x1), per workload, valid only for the kernel sources they were taken with.
+MEASURED_TRAFFIC = {
+    "frame400_n4_bf16": {"sources_sha256_16": "ae01b8acd3961482", "fetch_kib": 7656.9 * 2, "write_kib": 11760.0},
+}
+# the sources each measured kernel is built from
+KERNEL_SOURCES = {
+    "frame400_n4_bf16": ("paper_2103_03231_amd/csrc/render_kernel.h", "paper_2103_03231_amd/csrc/render_bf16_topn.hip",
+                         "paper_2103_03231_amd/csrc/layout.h", "paper_2103_03231_amd/csrc/internal.h"),
+    "targets400_b128_k5_z5": ("paper_2103_03231_amd/csrc/targets.hip", "paper_2103_03231_amd/csrc/internal.h"),
+}
 
 
-def kernel_sources_sha() -> str:
+def measured_traffic(workload):
+    """HBM bytes per dispatch if counters were taken for the current sources."""
+    m = MEASURED_TRAFFIC.get(workload)
+    if m is None or m["sources_sha256_16"] != kernel_sources_sha(workload):
+        return None
+    return round((m["fetch_kib"] + m["write_kib"]) * 1024)
+
+
+def kernel_sources_sha(workload: str = "frame400_n4_bf16") -> str:
     import hashlib
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in KERNEL_SOURCES[workload]:
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -109,6 +120,63 @@ def cpu_baseline(wl, weights, poses, n_sample):
                       f"os.cpu_count()={os.cpu_count()}"}
 
 
+def bench_targets(args, tw):
+    """Training targets (Sec. 5.1, Eq. 6-8) of the seeded depth maps: one
+    step is one donerf_targets call over all P maps.  HBM-bound: each pixel
+    reads its 4-byte depth once (the window re-reads hit L2) and writes
+    4 B bytes of targets."""
+    import torch
+
+    from paper_2103_03231_amd import binding as b
+    from paper_2103_03231_amd import inputs
+
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    r = b.Renderer(b.Config(n_bins=tw.n_bins), inputs.make_weights(tw.n_bins, 0))
+    depth_h = inputs.make_depth_maps(tw.P, tw.H, tw.W, tw.seed)
+    depth = torch.from_numpy(depth_h).cuda()
+    out = torch.empty((tw.P, tw.H, tw.W, tw.n_bins), dtype=torch.float32, device="cuda")
+    call = lambda: b.donerf_targets(r.h, depth.data_ptr(), tw.P, tw.H, tw.W, tw.K, tw.Z, out.data_ptr())
+    for _ in range(args.warmup):
+        call()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for e0, e1 in ev:
+        e0.record(stream)
+        call()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kern_ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in ev]))
+    ms_step = wall * 1e3 / args.steps
+    bytes_launch = tw.pixels * (4 + 4 * tw.n_bins)
+    achieved = bytes_launch / (kern_ms * 1e-3) / 1e9
+    line = {
+        "metric": "Mpixels/s of depth-oracle training targets (Eq. 6-8)",
+        "value": round(tw.pixels / (ms_step * 1e-3) / 1e6, 3), "unit": "Mpixels/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic: seeded z-buffered depth maps (tilted discs and rectangles over an empty background)",
+        "config": {"workload": tw.name, "maps": tw.P, "H": tw.H, "W": tw.W, "classes": tw.n_bins, "K": tw.K,
+                   "Z": tw.Z, "algorithmic_bytes_per_pixel": 4 + 4 * tw.n_bins},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": (round(sum(args.traffic_kib) * 1024) if args.traffic_kib else measured_traffic(tw.name)),
+                     "kernel": "targets_kernel", "kernel_ms": round(kern_ms, 4)},
+    }
+    if not args.no_cpu:
+        from oracle import targets_oracle as T
+        crop = depth_h[0, :200, :200]
+        t0 = time.perf_counter()
+        T.training_targets(crop, 0.1, 10.0, tw.n_bins, tw.K, tw.Z)
+        dt = time.perf_counter() - t0
+        line["cpu_baseline"] = {"value": crop.size / dt / 1e6, "unit": "Mpixels/s", "cores": 1, "kind": "oracle",
+                                "sample": f"one 200 x 200 crop of map 0, fp64 NumPy, {dt:.1f} s"}
+    r.close()
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -145,6 +213,8 @@ def main():
     from paper_2103_03231_amd import binding as b
     from paper_2103_03231_amd import inputs
 
+    if args.workload in inputs.TARGET_WORKLOADS:
+        return bench_targets(args, inputs.TARGET_WORKLOADS[args.workload])
     wl = inputs.WORKLOADS[args.workload]
     weights = inputs.make_weights(wl.n_bins, 0, wl.depth_input)
     poses = wl.poses()
@@ -186,13 +256,11 @@ def main():
     achieved = flop_launch / (avg_kern_ms * 1e-3) / 1e12
     peak = (mixed_peak(wl.N, wl.n_bins, d_in) if wl.precision == "fp8" else MFMA_PEAK_TFLOPS[wl.precision])
     paper_mrays = 400 * 400 / 22e-3 / 1e6   # 22 ms per 400x400 frame, N = 4
-    traffic = None
     kib = args.traffic_kib
-    if kib is None and (MEASURED_TRAFFIC["workload"] == wl.name
-                        and MEASURED_TRAFFIC["sources_sha256_16"] == kernel_sources_sha()):
-        kib = (MEASURED_TRAFFIC["fetch_kib"], MEASURED_TRAFFIC["write_kib"])
     if kib is not None:
         traffic = round((kib[0] + kib[1]) * 1024)
+    else:
+        traffic = measured_traffic(wl.name)
     line = {
         "metric": "Mrays/s + ms/frame at 400x400 N=4 (8x256 MLPs); MFMA util % of peak",
         "value": round(value, 3),

@@ -248,3 +248,27 @@ WORKLOADS = {
     "stereo1440x1600_n16_b256_bf16": Workload("stereo1440x1600_n16_b256_bf16", 1600, 1440,
                                               tuple(range(60)), 16, n_bins=256, stereo=True),
 }
+
+
+@dataclass(frozen=True)
+class TargetWorkload:
+    """Depth-oracle training targets for P synthetic depth maps of H x W."""
+
+    name: str
+    P: int
+    H: int
+    W: int
+    n_bins: int
+    K: int
+    Z: int
+    seed: int = 7
+
+    @property
+    def pixels(self) -> int:
+        return self.P * self.H * self.W
+
+
+TARGET_WORKLOADS = {
+    # the paper's K-5 Z-5 configuration at its 400 x 400 resolution, 128 classes
+    "targets400_b128_k5_z5": TargetWorkload("targets400_b128_k5_z5", 5, 400, 400, 128, 5, 5),
+}
