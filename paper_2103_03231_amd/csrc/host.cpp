@@ -501,9 +501,11 @@ int donerf_targets(donerf_t* h, const float* depth, int32_t P, int32_t H, int32_
     if (P < 1 || H < 1 || W < 1) return fail(DONERF_E_INVALID_ARG, "P, H and W must be >= 1");
     if (K < 1 || K > kTgtMaxK || Z < 1 || Z > kTgtMaxK)
         return fail(DONERF_E_INVALID_ARG, "K and Z must lie in [1, 15]");
-    if ((int64_t)P * H * ((W + 63) / 64) >= ((int64_t)1 << 31)) return fail(DONERF_E_INVALID_ARG, "too many pixels");
+    if ((int64_t)P * H * W >= ((int64_t)1 << 31)) return fail(DONERF_E_INVALID_ARG, "too many pixels");
     const int B = h->cfg.n_bins;
-    hipError_t e = launch_targets(depth, P, H, W, h->bins + 2 * B, B, K, Z, out, h->stream);
+    const float inv_l2span =
+        (float)(1.0 / std::log2((double)h->cfg.far_dist - (double)h->cfg.near_dist + 1.0));
+    hipError_t e = launch_targets(depth, P, H, W, h->bins + 2 * B, B, K, Z, inv_l2span, out, h->stream);
     if (e != hipSuccess) return hip_fail(e, "targets launch");
     return DONERF_OK;
 }

@@ -87,6 +87,6 @@ hipError_t launch_topn(bool bf16_layout, int ncap, const float* scores, int32_t 
 constexpr int kMaxBins = 256;
 constexpr int kTgtMaxK = 15;
 hipError_t launch_targets(const float* depth, int P, int H, int W, const float* bounds, int B, int K, int Z,
-                          float* out, hipStream_t stream);
+                          float inv_l2span, float* out, hipStream_t stream);
 
 }  // namespace donerf
