@@ -120,10 +120,18 @@ __device__ __forceinline__ void lds_barrier() {
 }
 
 constexpr int kChunkVec = kChunkBytes / 16;  // u32x4 per chunk
+// LDS fragment reads in flight, in MFMA steps: bf16 and fp32 steps read
+// one 1 KiB unit, fp8 steps two.  Measured on 5 x 400 x 400, N = 4: 12 bf16
+// steps ahead run 2 % faster than 3 (14 and more spill); fp8 layers run
+// best with 2 (of 2, 3, 4, 6).
 #ifndef DONERF_FRAG_AHEAD
-#define DONERF_FRAG_AHEAD 3
+#define DONERF_FRAG_AHEAD 12
 #endif
-constexpr int kFragAhead = DONERF_FRAG_AHEAD;  // LDS fragment reads in flight
+#ifndef DONERF_FRAG_AHEAD_FP8
+#define DONERF_FRAG_AHEAD_FP8 2
+#endif
+constexpr int kFragAhead = DONERF_FRAG_AHEAD;
+constexpr int kFragAheadFp8 = DONERF_FRAG_AHEAD_FP8;
 
 // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
 template <int VM>
@@ -322,7 +330,7 @@ __device__ __forceinline__ void hidden_layer(WS& st, int g, const float* bias, G
     constexpr int PF = KS * RBP;       // steps per pass
     constexpr int NF = 8 * KS;         // steps of the layer
     constexpr int SPC = kChunkFrags / U;  // steps per chunk
-    constexpr int D = kFragAhead;
+    constexpr int D = MP == kFP8 ? kFragAheadFp8 : kFragAhead;
     static_assert(OUT != kFP8 || RBP == 2, "an fp8 K step takes two row blocks");
     f32x16 acc[2][RBP][CB];
     u32x4 a[D + 1][U];
@@ -805,13 +813,16 @@ render_kernel(const RenderArgs a) {
     // Head of the depth network: B / 64 passes of 64 classes (32 * kRbPerPass).
     const int npass = a.B / (32 * kRbPerPass);
     constexpr int PASS_FRAGS = KS_H * kRbPerPass;
-    // A pass spans CPP whole chunks; GP passes make an even number of them
-    // (the head is padded to even chunks, so a missing pass of an odd count
-    // is the padding chunk).
-    static_assert(PASS_FRAGS % kChunkFrags == 0, "a pass spans whole chunks");
-    constexpr int CPP = PASS_FRAGS / kChunkFrags;
-    constexpr int GP = CPP % 2 == 0 ? 1 : 2;
-    static_assert(CPP % 2 == 0 || CPP == 1, "pass grouping");
+    // Passes are grouped so that a group spans exactly two chunks (a pass
+    // spans CPP whole chunks, or PPC passes share one); the head is padded to
+    // an even number of chunks, so the chunks of a missing pass that starts a
+    // chunk are padding and are consumed in its place.
+    static_assert(PASS_FRAGS >= kChunkFrags ? PASS_FRAGS % kChunkFrags == 0 : kChunkFrags % PASS_FRAGS == 0,
+                  "passes and chunks nest");
+    constexpr int CPP = PASS_FRAGS >= kChunkFrags ? PASS_FRAGS / kChunkFrags : 1;
+    constexpr int PPC = PASS_FRAGS >= kChunkFrags ? 1 : kChunkFrags / PASS_FRAGS;
+    static_assert(CPP <= 2, "pass grouping");
+    constexpr int GP = CPP == 2 ? 1 : 2 * PPC;
     auto dump_scores = [&](int p, int R, int C, const f32x16& acc) {
         if (a.out_scores && part == 0 && valid[C]) {
             float* dst = a.out_scores + (size_t)rid[C] * a.B;
@@ -831,7 +842,10 @@ render_kernel(const RenderArgs a) {
                 constexpr int q = CV(Q);
                 const int p = p0 + q;
                 if (p >= npass) {
-                    if constexpr (CPP == 1) st.template next<q & 1>();   // padding chunk
+                    constexpr int f0 = q * PASS_FRAGS;   // the pass's first fragment in the group
+                    if constexpr (f0 % kChunkFrags == 0) {
+                        sfor<CPP>([&](auto J) { st.template next<(f0 / kChunkFrags + CV(J)) & 1>(); });
+                    }
                 } else {
                     run_pass<FP, CB, KS_H, kRbPerPass, q * PASS_FRAGS>(
                         st, g, bias_s + 7 * 256 + 32 * kRbPerPass * p, g0, [&](auto R, auto C, const f32x16& acc) {
@@ -851,6 +865,7 @@ render_kernel(const RenderArgs a) {
     } else {
         // Inverse-CDF placement needs every class value of the ray; B <= 128
         // keeps them in registers (the hidden activations h1 are dead here).
+        static_assert(PASS_FRAGS % kChunkFrags == 0, "a pass spans whole chunks");
         constexpr int NPM = 128 / (32 * kRbPerPass);
         float vals[CB][NPM][kRbPerPass][16];
         sfor<NPM>([&](auto PI) {
