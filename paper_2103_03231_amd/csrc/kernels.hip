@@ -61,9 +61,10 @@ __global__ void __launch_bounds__(256) topn_kernel(const float* scores, int32_t 
             for (int R = 0; R < 2; ++R)
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
-                    const int c = 64 * p + 32 * R + 8 * (i / 4) + 4 * g + (i % 4);
-                    t.push_ascending(row[c], c);
+                    const int c = 64 * p + 32 * R + 8 * (i / 4) + (i % 4);
+                    t.push(row[c + 4 * g], c);
                 }
+        t.rebase(4 * g);
         t.merge_partner();
         int s[NCAP];
         t.ascending(N, s);

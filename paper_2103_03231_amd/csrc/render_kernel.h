@@ -396,59 +396,66 @@ __device__ __forceinline__ void hidden_layer(WS& st, int g, const float* bias, G
 // ------------------------------------------------------------------ selection
 
 // Best-first list of (score, class) under the order: higher score first,
-// lower class index first among equal scores.
+// lower class index first among equal scores, -0 equal to +0, NaN below
+// every number.  Each entry is one 64-bit key that orders exactly like that:
+// the score's bits mapped to an unsigned order (the sign bit flipped for
+// numbers >= +0, every bit flipped below), then 20 bits of 0xFFFFF - class.
+// With the exponent of 1.0 above them the keys are doubles in [1, 2) whose
+// numeric order is the key order, so an insertion is a max/min chain of
+// v_max_f64 / v_min_f64: no compare masks and no branches, where a
+// compare-and-select list needs four masks per insertion.  The list starts
+// with keys of 1.0, below every real key.
 template <int NCAP>
 struct TopList {
-    float v[NCAP];
-    int i[NCAP];
+    static constexpr uint32_t kIdx = 0xFFFFFu;
+    double v[NCAP];
     __device__ __forceinline__ void init() {
 #pragma unroll
+        for (int k = 0; k < NCAP; ++k) v[k] = 1.0;
+    }
+    __device__ static __forceinline__ double key(float x, uint32_t cidx) {
+        const uint32_t u = __float_as_uint(x + 0.0f);   // -0 becomes +0; NaN stays NaN
+        uint32_t ord = u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u);
+        ord = x != x ? 0u : ord;
+        const uint32_t hi = __builtin_amdgcn_alignbit(0x3FFu, ord, 12);   // 0x3FF00000 | ord >> 12
+        const uint32_t lo = (ord << 20) | cidx;
+        return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+    }
+    __device__ __forceinline__ void insert(double t) {
+#pragma unroll
         for (int k = 0; k < NCAP; ++k) {
-            v[k] = -INFINITY;
-            i[k] = 0x7fff;
+            const double hi = __builtin_fmax(v[k], t);
+            if (k + 1 < NCAP) t = __builtin_fmin(v[k], t);
+            v[k] = hi;
         }
     }
-    __device__ __forceinline__ void place(const bool (&c)[NCAP], float x, int ix) {
-        // c is monotone (c[k] implies c[k+1]); shift the tail down by one.
+    // Insert class ix - off of score x: callers pass the wave-uniform part
+    // of the class index here and its lane part (off) to rebase() once all
+    // classes are in; the order within the lane is the same.
+    __device__ __forceinline__ void push(float x, int ix) { insert(key(x, kIdx - (uint32_t)ix)); }
+    // Classes become ix + off.  Every key is a real one by then (each lane
+    // pushes at least NCAP classes), so the index field does not wrap.
+    __device__ __forceinline__ void rebase(int off) {
 #pragma unroll
-        for (int k = NCAP - 1; k > 0; --k) {
-            v[k] = c[k - 1] ? v[k - 1] : (c[k] ? x : v[k]);
-            i[k] = c[k - 1] ? i[k - 1] : (c[k] ? ix : i[k]);
-        }
-        v[0] = c[0] ? x : v[0];
-        i[0] = c[0] ? ix : i[0];
+        for (int k = 0; k < NCAP; ++k)
+            v[k] = __builtin_bit_cast(double, __builtin_bit_cast(uint64_t, v[k]) - (uint64_t)(uint32_t)off);
     }
-    // Insert a class whose index exceeds every index already held.
-    __device__ __forceinline__ void push_ascending(float x, int ix) {
-        bool c[NCAP];
-#pragma unroll
-        for (int k = 0; k < NCAP; ++k) c[k] = x > v[k];
-        place(c, x, ix);
-    }
-    // Insert any class.
-    __device__ __forceinline__ void push(float x, int ix) {
-        bool c[NCAP];
-#pragma unroll
-        for (int k = 0; k < NCAP; ++k) c[k] = x > v[k] || (x == v[k] && ix < i[k]);
-        place(c, x, ix);
+    __device__ __forceinline__ int index(int k) const {
+        return (int)(kIdx - ((uint32_t)__builtin_bit_cast(uint64_t, v[k]) & kIdx));
     }
     // Merge with the list of lane l ^ 32 (the other half of the same ray's
     // classes); both lanes end with the same list.
     __device__ __forceinline__ void merge_partner() {
-        float pv[NCAP];
-        int pi[NCAP];
+        double pv[NCAP];
 #pragma unroll
-        for (int k = 0; k < NCAP; ++k) {
-            pv[k] = __shfl_xor(v[k], 32);
-            pi[k] = __shfl_xor(i[k], 32);
-        }
+        for (int k = 0; k < NCAP; ++k) pv[k] = __shfl_xor(v[k], 32);
 #pragma unroll
-        for (int k = 0; k < NCAP; ++k) push(pv[k], pi[k]);
+        for (int k = 0; k < NCAP; ++k) insert(pv[k]);
     }
     // The first N classes in ascending index order in s[0..N), padding after.
     __device__ __forceinline__ void ascending(int N, int (&s)[NCAP]) const {
 #pragma unroll
-        for (int k = 0; k < NCAP; ++k) s[k] = k < N ? i[k] : 0x7fff;
+        for (int k = 0; k < NCAP; ++k) s[k] = k < N ? index(k) : 0x7fff;
 #pragma unroll
         for (int round = 0; round < NCAP; ++round) {
 #pragma unroll
@@ -849,16 +856,16 @@ render_kernel(const RenderArgs a) {
                 } else {
                     run_pass<FP, CB, KS_H, kRbPerPass, q * PASS_FRAGS>(
                         st, g, bias_s + 7 * 256 + 32 * kRbPerPass * p, g0, [&](auto R, auto C, const f32x16& acc) {
-                            const int rowb = 32 * kRbPerPass * p + 32 * CV(R) + 4 * g;
+                            const int rowb = 32 * kRbPerPass * p + 32 * CV(R);   // + 4 g: rebase below
 #pragma unroll
-                            for (int i = 0; i < 16; ++i)
-                                top[CV(C)].push_ascending(acc[i], rowb + 8 * (i / 4) + (i % 4));
+                            for (int i = 0; i < 16; ++i) top[CV(C)].push(acc[i], rowb + 8 * (i / 4) + (i % 4));
                             dump_scores(p, CV(R), CV(C), acc);
                         });
                 }
             });
         }
         sfor<CB>([&](auto C) {
+            top[CV(C)].rebase(4 * g);
             top[CV(C)].merge_partner();
             top[CV(C)].ascending(a.N, sel[CV(C)]);
         });

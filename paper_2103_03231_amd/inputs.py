@@ -178,6 +178,8 @@ def random_logits(rays: int, n_bins: int, seed: int, mode: str = "normal") -> np
     mode 'ties'   - values quantised to a few levels, so rows hold many ties,
                     including +0 and -0
     mode 'const'  - every value of a row equal
+    mode 'special' - the 'ties' levels mixed with NaN, +inf and -inf (about
+                    one value in eight each)
     """
     rng = SplitMix64(0x70F + seed)
     if mode == "normal":
@@ -189,6 +191,13 @@ def random_logits(rays: int, n_bins: int, seed: int, mode: str = "normal") -> np
         out = (q * 0.25).astype(np.float32)
         signs = rng.uniform(rays * n_bins).reshape(rays, n_bins) < 0.5
         out[(out == 0) & signs] = np.float32(-0.0)
+        return out
+    if mode == "special":
+        out = random_logits(rays, n_bins, seed, "ties")
+        pick = SplitMix64(0x5EC1A1 + seed).uniform(rays * n_bins).reshape(rays, n_bins)
+        out[pick < 0.125] = np.float32(np.nan)
+        out[(pick >= 0.125) & (pick < 0.25)] = np.float32(np.inf)
+        out[(pick >= 0.25) & (pick < 0.375)] = np.float32(-np.inf)
         return out
     if mode == "const":
         v = (rng.uniform(rays) * 4.0 - 2.0).astype(np.float32)

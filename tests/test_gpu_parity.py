@@ -90,7 +90,7 @@ def test_bin_table_bit_exact(B):
 @pytest.mark.parametrize("B", [64, 128, 192, 256])
 def test_topn_bit_exact(precision, B):
     r, _ = renderer(precision, n_bins=B, n_max=16)
-    for mode in ("normal", "ties", "const"):
+    for mode in ("normal", "ties", "const", "special"):
         lg = inputs.random_logits(3001, B, seed=B, mode=mode)
         dev = torch.from_numpy(lg).cuda()
         for N in (1, 3, 4, 5, 8, 16):

@@ -263,12 +263,16 @@ def test_flops_reproduce_paper_table2():
 
 def test_topn_matches_sorted_brute_force():
     rng = np.random.default_rng(7)
-    for mode in ("normal", "ties", "const"):
+    for mode in ("normal", "ties", "const", "special"):
         lg = inputs.random_logits(300, 16, seed=3, mode=mode)
         for N in (1, 2, 4, 8, 16):
             got = O.topn(lg, N)
             for r in range(lg.shape[0]):
-                ref = sorted(sorted(range(16), key=lambda i: (-float(lg[r, i]), i))[:N])
+                # NaN after every number (-inf included), then by index
+                def rank(i):
+                    x = float(lg[r, i])
+                    return (1, 0.0, i) if math.isnan(x) else (0, -x, i)
+                ref = sorted(sorted(range(16), key=rank)[:N])
                 assert list(got[r]) == ref
     lg = rng.permutation(64).astype(F32)[None, :]
     assert list(O.topn(lg, 5)[0]) == sorted(np.argsort(-lg[0])[:5])
