@@ -53,6 +53,8 @@ def test_one_hot_classes_bit_exact(B):
     (256, 5, 1, 1, 12, 40),
     (128, 1, 5, 1, 9, 65),
     (64, 15, 15, 1, 11, 17),
+    (192, 13, 7, 1, 14, 45),   # three window entries per lane, three classes per lane
+    (128, 11, 1, 1, 13, 29),
     (128, 5, 5, 1, 1, 100),
     (128, 7, 3, 1, 1, 1),
 ])
