@@ -392,6 +392,34 @@ def test_depth_input_features_match_oracle():
     r.close()
 
 
+def test_depth_input_features_bf16_match_oracle():
+    """The bf16 path's encoding (the hardware sine and cosine after exact
+    reduction to [-1/2, 1/2] revolutions) read back through the same exact
+    pass-through network: every step is exact in bf16 (weights +-1, identity
+    layers, ReLU of bf16 values), so the scores are the bf16-rounded
+    features.  The oracle rounds its exact features the same way: identity
+    slots agree bit for bit; a sin/cos slot may round the other way only when
+    its exact value lies within the encoding's error of a rounding midpoint,
+    so mismatches must be rare and exactly one bf16 step apart."""
+    blob = _feature_probe_blob()
+    r = b.Renderer(b.Config(n_bins=128, n_max=4, precision=b.BF16), blob)
+    poses = inputs.make_poses([0, 9])
+    g = gpu_render(r, poses, 23, 29, 4)
+    feats = g["scores"].reshape(-1, 128)[:, :90].astype(np.float32)
+    ref = O.render(blob, poses, 23, 29, 4, precision="bf16")["logits"][:, :90].astype(np.float32)
+    ident = [0, 1, 2, 63, 64, 65]
+    assert np.array_equal(feats[:, ident], ref[:, ident])
+    # adjacent bf16 values: the fp32 bit patterns differ by one unit in bit 16
+    gb = feats.view(np.int32).astype(np.int64)
+    rb = ref.view(np.int32).astype(np.int64)
+    diff = gb != rb
+    frac = diff.mean()
+    log(f"[depth features bf16] mismatched {diff.sum()} of {diff.size} ({frac:.2e})")
+    assert frac <= 1e-3, frac
+    assert np.all(np.abs(gb[diff] - rb[diff]) == 1 << 16) and np.all(np.sign(feats[diff]) * np.sign(ref[diff]) >= 0)
+    r.close()
+
+
 # ------------------------------------------------------------------ the paper's unencoded depth input
 
 def _position_probe_blob(B, cols):
