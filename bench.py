@@ -284,6 +284,9 @@ def main():
                    "padded_mflop_per_ray": round(padded_flop_per_ray(wl.N, wl.n_bins, d_in) / 1e6, 4)},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(achieved / peak, 4),
+                     # the same launch counted by the tile work the MFMAs execute (padding included)
+                     "padded_frac": round(padded_flop_per_ray(wl.N, wl.n_bins, d_in) * rays
+                                          / (avg_kern_ms * 1e-3) / 1e12 / peak, 4),
                      **({"peak_note": "fp8 hidden layers at 5000, bf16 first layers and heads at 2500, "
                                       "combined by their share of the work"} if wl.precision == "fp8" else {}),
                      "traffic": traffic,
