@@ -142,6 +142,8 @@ def test_bf16_small_frames_against_bf16_oracle():
     (8, 256, 16, 24, 1),
     (16, 256, 12, 20, 1),
     (4, 192, 3, 5, 35),       # more poses than one launch holds
+    (1, 128, 1, 1, 1),        # a single ray: one tile of 255 idle columns
+    (4, 128, 1, 1, 1),        # a single ray split four ways by samples, then combined
 ])
 def test_variants(precision, N, B, H, W, P):
     r, w = renderer(precision, n_bins=B, n_max=max(N, 4))
@@ -198,6 +200,53 @@ def test_render_rejects_bad_sample_count():
         b.donerf_render(r.h, bad, 1, 8, 8, 4, out["rgb"].data_ptr())
     assert e.value.status == b.E_NONFINITE
     r.close()
+
+
+def test_render_rejects_bad_sizes():
+    """Empty frames and frames beyond the stated limits (P H W < 2^31,
+    H W <= 2^24) fail before any launch."""
+    r, _ = renderer("bf16", n_max=4)
+    out = r.alloc(1, 2, 2, 4)
+    for P, H, W in ((0, 8, 8), (1, 0, 8), (1, 8, -1), (200, 4096, 4096), (1, 8192, 8192)):
+        poses = inputs.make_poses(list(range(max(P, 1))))
+        with pytest.raises(b.DonerfError) as e:
+            b.donerf_render(r.h, poses, P, H, W, 4, out["rgb"].data_ptr())
+        assert e.value.status == b.E_INVALID_ARG, (P, H, W)
+    r.close()
+
+
+def _shading_sigma(blob, weight, bias):
+    """The blob with the shading head's density row (its last output) set to
+    constant weights and bias."""
+    w = blob.copy()
+    n_in = 256 + 27
+    row = len(w) - 4 - 4 * n_in + 3 * n_in
+    w[row:row + n_in] = weight
+    w[-1] = bias
+    return w
+
+
+@pytest.mark.parametrize("precision", ["fp32", "bf16", "fp8"])
+def test_transparent_and_opaque_scenes(precision):
+    """Closed forms of the compositing: with density 0 everywhere nothing is
+    accumulated (RGB and depth exactly 0, black background); with a density
+    so large that the first sample's opacity is 1 in fp32, the depth is
+    exactly the first sample's depth, the centre of the lowest selected
+    class."""
+    prec = {"fp32": b.FP32, "bf16": b.BF16, "fp8": b.FP8}[precision]
+    base = inputs.make_weights(128, 0)
+    poses = inputs.make_poses([0, 5])
+    for sigma_bias, opaque in ((-1.0, False), (1e4, True)):
+        r = b.Renderer(b.Config(n_bins=128, n_max=4, precision=prec), _shading_sigma(base, 0.0, sigma_bias))
+        _, centres, _ = b.donerf_debug_bins(r.h, 128)
+        g = gpu_render(r, poses, 19, 21, 4)
+        if not opaque:
+            assert np.all(g["rgb"] == 0.0) and np.all(g["depth"] == 0.0)
+        else:
+            first = g["bins"].reshape(-1, 4)[:, 0]
+            assert np.array_equal(g["depth"].reshape(-1), centres[first])
+            assert np.all((g["rgb"] >= 0.0) & (g["rgb"] <= 1.0)) and g["rgb"].max() > 0.0
+        r.close()
 
 
 # ------------------------------------------------------------------ full-size workloads, sampled
