@@ -104,4 +104,9 @@ def test_rejects_bad_windows():
         with pytest.raises(b.DonerfError) as e:
             b.donerf_targets(r.h, d.data_ptr(), 1, 4, 4, K, Z, out.data_ptr())
         assert e.value.status == b.E_INVALID_ARG
+    # empty maps and more than 2^31 pixels fail before any launch
+    for P, H, W in ((0, 4, 4), (1, 0, 4), (1, 4, 0), (128, 4096, 4096)):
+        with pytest.raises(b.DonerfError) as e:
+            b.donerf_targets(r.h, d.data_ptr(), P, H, W, 5, 5, out.data_ptr())
+        assert e.value.status == b.E_INVALID_ARG, (P, H, W)
     r.close()
