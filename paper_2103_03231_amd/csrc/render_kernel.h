@@ -670,6 +670,28 @@ __device__ __forceinline__ void fourier(const float (&v)[3], int g, float* f) {
     }
 }
 
+// ------------------------------------------------------------------ scalar functions
+
+// exp(-x), 1 / (1 + exp(-x)) and 1 - exp(-x): correctly rounded library
+// functions for the fp32 network; for bf16 and fp8 networks the hardware
+// exponential (v_exp_f32 on x log2 e) and reciprocal (v_rcp_f32), each within
+// about an ulp, far inside what those networks' roundings already move.
+template <bool EXACT>
+__device__ __forceinline__ float exp_neg(float x) {
+    if constexpr (EXACT) return expf(-x);
+    else return __builtin_amdgcn_exp2f(x * -1.4426950408889634f);
+}
+template <bool EXACT>
+__device__ __forceinline__ float sigmoid(float x) {
+    if constexpr (EXACT) return 1.0f / (1.0f + expf(-x));
+    else return __builtin_amdgcn_rcpf(1.0f + exp_neg<false>(x));
+}
+template <bool EXACT>
+__device__ __forceinline__ float one_minus_exp_neg(float x) {
+    if constexpr (EXACT) return -expm1f(-x);
+    else return 1.0f - exp_neg<false>(x);
+}
+
 // ------------------------------------------------------------------ fused kernel
 
 constexpr int kBiasMax = 7 * 256 + 256 + 7 * 256 + 32;
@@ -881,7 +903,7 @@ render_kernel(const RenderArgs a) {
                 run_pass<FP, CB, KS_H, kRbPerPass, p * PASS_FRAGS>(
                     st, g, bias_s + 7 * 256 + 32 * kRbPerPass * p, g0, [&](auto R, auto C, const f32x16& acc) {
 #pragma unroll
-                        for (int i = 0; i < 16; ++i) vals[CV(C)][p][CV(R)][i] = 1.0f / (1.0f + expf(-acc[i]));
+                        for (int i = 0; i < 16; ++i) vals[CV(C)][p][CV(R)][i] = sigmoid<FP == kF32>(acc[i]);
                         dump_scores(p, CV(R), CV(C), acc);
                     });
             } else {
@@ -949,18 +971,18 @@ render_kernel(const RenderArgs a) {
             st, g, bias_s + s_bias + 7 * 256, gh, [&](auto R, auto C, const f32x16& acc) {
                 constexpr int cb = CV(C);
                 // lanes of group 0 hold rows 0..3 = (r, g, b, sigma) in registers 0..3
-                const float cr = 1.0f / (1.0f + expf(-acc[0]));
-                const float cg = 1.0f / (1.0f + expf(-acc[1]));
-                const float cbl = 1.0f / (1.0f + expf(-acc[2]));
+                const float cr = sigmoid<FP == kF32>(acc[0]);
+                const float cg = sigmoid<FP == kF32>(acc[1]);
+                const float cbl = sigmoid<FP == kF32>(acc[2]);
                 const float sigma = fmaxf(acc[3], 0.0f);
                 const float tau = sigma * dk[cb];
-                const float alpha = -expm1f(-tau);
+                const float alpha = one_minus_exp_neg<FP == kF32>(tau);
                 const float wgt = T[cb] * alpha;
                 Cr[cb] += wgt * cr;
                 Cg[cb] += wgt * cg;
                 Cb[cb] += wgt * cbl;
                 Dp[cb] += wgt * tk[cb];
-                T[cb] *= expf(-tau);
+                T[cb] *= exp_neg<FP == kF32>(tau);
             });
         // the shading head is padded to an even number of chunks
         if constexpr ((((KS_H + KS_SK) + kChunkFrags - 1) / kChunkFrags) & 1) st.template next<1>();
