@@ -31,7 +31,7 @@ HBM_PEAK_GBS = 8000.0
 # 256 MiB copy (FETCH_SIZE reads half the bytes moved: x2; WRITE_SIZE exact:
 # x1), per workload, valid only for the kernel sources they were taken with.
 MEASURED_TRAFFIC = {
-    "frame400_n4_bf16": {"sources_sha256_16": "b98427c33f6c3d70", "fetch_kib": 7554.5 * 2, "write_kib": 11760.0},
+    "frame400_n4_bf16": {"sources_sha256_16": "0cdb203e9d6367fc", "fetch_kib": 7549.5 * 2, "write_kib": 11760.0},
     "targets400_b128_k5_z5": {"sources_sha256_16": "9372bf38b91fcebc", "fetch_kib": 9069.9 * 2, "write_kib": 400000.0},
 }
 # the sources each measured kernel is built from
