@@ -202,6 +202,31 @@ def test_render_rejects_bad_sample_count():
     r.close()
 
 
+def test_render_on_a_side_stream():
+    """The handle's stream carries the launches: a render queued on a second
+    stream behind a fill of its output equals the default-stream render bit
+    for bit, and so do the training targets."""
+    r, _ = renderer("bf16", n_max=4)
+    poses = inputs.make_poses([2, 3])
+    ref = r.render(poses, 33, 47, 4, depth=True)
+    d = torch.from_numpy(inputs.make_depth_maps(1, 40, 70, 11)).cuda()
+    tref = r.targets(d, 5, 5)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    out = r.alloc(2, 33, 47, 4, depth=True)
+    with torch.cuda.stream(side):
+        b.donerf_set_stream(r.h, side.cuda_stream)
+        out["rgb"].fill_(-1.0)
+        out["depth"].fill_(-1.0)
+        r.render_into(poses, 33, 47, 4, out)
+        t = r.targets(d, 5, 5)
+    side.synchronize()
+    b.donerf_set_stream(r.h, torch.cuda.current_stream().cuda_stream)
+    assert torch.equal(out["rgb"], ref["rgb"]) and torch.equal(out["depth"], ref["depth"])
+    assert torch.equal(t, tref)
+    r.close()
+
+
 def test_render_rejects_bad_sizes():
     """Empty frames and frames beyond the stated limits (P H W < 2^31,
     H W <= 2^24) fail before any launch."""
