@@ -54,7 +54,9 @@ typedef enum donerf_status {
 typedef enum donerf_precision {
     DONERF_FP32 = 0, /* fp32 weights, features and activations, fp32 MFMA    */
     DONERF_BF16 = 1, /* bf16 weights, features and hidden activations (RNE),
-                        fp32 accumulation, fp32 scores, heads, compositing   */
+                        fp32 accumulation, fp32 scores, heads, compositing;
+                        sine, cosine, exp and reciprocal of the encoding and
+                        compositing from the hardware instructions           */
     DONERF_FP8 = 2   /* the lower bit width Sec. 6.1 leaves as headroom: the
                         six hidden layers of each network in OCP E4M3 (weights
                         W 2^s rounded to nearest even with the largest s that
@@ -169,7 +171,8 @@ int donerf_set_stream(donerf_t* h, void* stream);
  * The work is enqueued on the handle's stream; results are valid once the
  * stream has been synchronised.  No allocation, no host synchronisation.
  * Errors: E_INVALID_ARG (NULL handle/poses/out_rgb, P, H, W < 1, N out of
- * range, P*H*W >= 2^31), E_NONFINITE (pose), E_HIP (launch failed).
+ * range, P*H*W >= 2^31, H*W > 2^24), E_NONFINITE (pose), E_HIP (launch
+ * failed).
  */
 int donerf_render(donerf_t* h, const float* cam_poses, int32_t P, int32_t H, int32_t W,
                   int32_t N, float* out_rgb, float* out_depth);
@@ -190,10 +193,10 @@ int donerf_render_debug(donerf_t* h, const float* cam_poses, int32_t P, int32_t 
 
 /*
  * Run the device top-N selection on given scores, for testing.
- *   scores   device, rays x B fp32, finite
+ *   scores   device, rays x B fp32
  *   out_idx  device, rays x N int32: the N classes with the highest scores,
  *            ties broken towards the lower class index, +0 and -0 equal,
- *            written in ascending class order
+ *            NaN below every number, written in ascending class order
  * Errors: E_INVALID_ARG (NULL, rays < 1, N out of range), E_HIP.
  */
 int donerf_debug_topn(donerf_t* h, const float* scores, int32_t rays, int32_t N,
@@ -212,7 +215,8 @@ int donerf_debug_topn(donerf_t* h, const float* scores, int32_t rays, int32_t N,
  *          / (floor(Z/2) + 1), 1) (classes outside [0, B) left out).
  *   depth  device, P x H x W fp32: the distance from the camera to the first
  *          surface along each pixel's ray (Eq. 1's d), row-major
- *   K, Z   window sizes, 1..15 (the paper uses 5 and 9)
+ *   K, Z   window sizes, 1..15 (the paper evaluates 1, 5 and 9 and uses
+ *          K = Z = 5)
  *   out    device, P x H x W x B fp32, caller-owned; B = cfg.n_bins
  * Enqueued on the handle's stream; no allocation.
  * Errors: E_INVALID_ARG (NULL, P, H, W < 1, K or Z out of range, too many
