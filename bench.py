@@ -204,7 +204,7 @@ def main():
         print(json.dumps({"copy_calibration_bytes_read": n * 4, "bytes_written": n * 4, "repeats": 3}))
         return
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only: the rays of a frame are "
+        print(json.dumps({"error": "the library runs on one GPU only: the rays of a frame are "
                                    "independent, so several GPUs would each render a share of the "
                                    "image; only --gpus 1 is measured"}))
         sys.exit(2)

@@ -48,7 +48,7 @@ typedef enum donerf_status {
     DONERF_E_DEVICE = -4,      /* no HIP device, or the device is not gfx950 */
     DONERF_E_NOMEM = -5,       /* device or host allocation failed           */
     DONERF_E_HIP = -6,         /* a HIP call failed; see donerf_last_error() */
-    DONERF_E_UNSUPPORTED = -7  /* valid request this build does not handle   */
+    DONERF_E_UNSUPPORTED = -7  /* valid request the library does not handle */
 } donerf_status;
 
 typedef enum donerf_precision {
@@ -104,7 +104,7 @@ typedef struct donerf_cfg {
     float far_dist;    /* d_max > d_min: farthest depth; also the normalisation
                           of Eq. 2 and the warp scale of Eq. 5                 */
     int32_t n_bins;    /* B: number of logarithmic depth classes (Eq. 3);
-                          this build supports 64, 128, 192 and 256            */
+                          the library supports 64, 128, 192 and 256          */
     int32_t n_max;     /* largest N a render may request, 1..16, n_max <= B   */
     float fov_x_deg;   /* horizontal field of view of the pinhole camera, in
                           degrees, 0 < fov < 180                               */
