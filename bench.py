@@ -34,11 +34,14 @@ MEASURED_TRAFFIC = {
     "frame400_n4_bf16": {"sources_sha256_16": "0cdb203e9d6367fc", "fetch_kib": 7549.5 * 2, "write_kib": 11760.0},
     "targets400_b128_k5_z5": {"sources_sha256_16": "9372bf38b91fcebc", "fetch_kib": 9069.9 * 2, "write_kib": 400000.0},
 }
-# the sources each measured kernel is built from
+# the sources (and the build script, whose flags shape the code) each
+# measured kernel is built from
 KERNEL_SOURCES = {
     "frame400_n4_bf16": ("paper_2103_03231_amd/csrc/render_kernel.h", "paper_2103_03231_amd/csrc/render_bf16_topn.hip",
-                         "paper_2103_03231_amd/csrc/layout.h", "paper_2103_03231_amd/csrc/internal.h"),
-    "targets400_b128_k5_z5": ("paper_2103_03231_amd/csrc/targets.hip", "paper_2103_03231_amd/csrc/internal.h"),
+                         "paper_2103_03231_amd/csrc/layout.h", "paper_2103_03231_amd/csrc/internal.h",
+                         "paper_2103_03231_amd/build.py"),
+    "targets400_b128_k5_z5": ("paper_2103_03231_amd/csrc/targets.hip", "paper_2103_03231_amd/csrc/internal.h",
+                              "paper_2103_03231_amd/build.py"),
 }
 
 

@@ -24,6 +24,15 @@ COMMON = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-ffp-contract=
           "-I", os.path.join(os.path.dirname(PKG), "include")]
 
 
+# Per-unit scheduling: the bf16 render units run 0.6 % faster with the
+# iterative ILP machine scheduler (measured on the 5 x 400 x 400 step); the
+# fp8 unit measured the same either way and keeps the default.
+UNIT_FLAGS = {
+    "render_bf16_topn.hip": ["-mllvm", "-amdgpu-sched-strategy=iterative-ilp"],
+    "render_bf16_cdf.hip": ["-mllvm", "-amdgpu-sched-strategy=iterative-ilp"],
+}
+
+
 def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
@@ -49,7 +58,7 @@ def build(verbose: bool = False, extra: list | None = None) -> str:
     for src in srcs:
         obj = os.path.join(bdir, src + ".o")
         lang = ["-x", "hip"] if src.endswith(".hip") else []
-        cmds.append([hipcc, *COMMON, *extra, *lang, "-c", os.path.join(CSRC, src), "-o", obj])
+        cmds.append([hipcc, *COMMON, *UNIT_FLAGS.get(src, []), *extra, *lang, "-c", os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)
     # translation units compile independently; keep a few in flight
     jobs = max(1, min(len(cmds), int(os.environ.get("MAX_JOBS", "0") or 0) or (os.cpu_count() or 1), 6))
