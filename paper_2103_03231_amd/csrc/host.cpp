@@ -386,7 +386,7 @@ int donerf_create(const donerf_cfg* cfg, const float* weights, size_t n_weights,
     std::vector<float> bounds, centres, widths;
     make_bins(*cfg, bounds, centres, widths);
     std::vector<uint8_t> frags;
-    std::vector<float> bias;
+    std::vector<float> bias, head_bias;
     int n_d_chunks = 0, n_s_chunks = 0;
     int32_t wscale[16];
     size_t off = 0;
@@ -407,11 +407,14 @@ int donerf_create(const donerf_cfg* cfg, const float* weights, size_t n_weights,
         }
         (l < 8 ? n_d_chunks : n_s_chunks) += layer_chunks(prec, kind, B);
         off += blob_w_count(l, B, cfg->depth_input);
-        const size_t b0 = bias.size();
-        bias.resize(b0 + bias_len(kind, B), 0.0f);
-        std::memcpy(bias.data() + b0, weights + off, sizeof(float) * lg.out_rows);
+        // the depth head's bias (B-dependent length) goes last
+        std::vector<float>& dst = l == 7 ? head_bias : bias;
+        const size_t b0 = dst.size();
+        dst.resize(b0 + bias_len(kind, B), 0.0f);
+        std::memcpy(dst.data() + b0, weights + off, sizeof(float) * lg.out_rows);
         off += lg.out_rows;
     }
+    bias.insert(bias.end(), head_bias.begin(), head_bias.end());
 
     donerf_t* h = new (std::nothrow) donerf_handle();
     if (!h) return fail(DONERF_E_NOMEM, "host allocation failed");

@@ -13,7 +13,7 @@ namespace donerf {
 struct RenderArgs {
     const uint4* d_frags;   // depth network fragments, chunk-padded per layer
     const uint4* s_frags;   // shading network fragments, chunk-padded per layer
-    const float* bias;      // all biases (layout.h bias_len), depth then shading
+    const float* bias;      // all biases (layout.h bias_len); the depth head's last
     const float* bins;      // centres[B] then widths[B]
     float* out_rgb;         // rays x 3
     float* out_depth;       // rays, or null

@@ -170,8 +170,9 @@ DN_HD constexpr int layer_chunks(int net, int kind, int n_bins) {
     return (layer_frags(net, kind, n_bins) + 2 * kChunkFrags - 1) / (2 * kChunkFrags) * 2;
 }
 
-// Bias table: every layer's bias padded to 32 * rb floats, depth layers
-// then shading layers.
+// Bias table: every layer's bias padded to 32 * rb floats; the depth
+// network's seven ReLU layers, the shading network's eight layers, then the
+// depth head (the one length that depends on B).
 DN_HD constexpr int bias_len(int kind, int n_bins) { return 32 * layer_geom(kind, n_bins).rb; }
 
 }  // namespace donerf

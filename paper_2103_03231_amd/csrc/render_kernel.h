@@ -208,13 +208,23 @@ struct WeightStream {
 
 // ------------------------------------------------------------------ MFMA layers
 
+// A layer's biases: element off of the workgroup's LDS bias array.  Reads
+// index the array itself with one integer offset: address arithmetic that
+// passes through loop-carried pointers loses the array's identity, and the
+// compiler then makes each such read wait for every LDS copy in flight.
+struct BiasAt {
+    const float* s;
+    int off;
+    __device__ __forceinline__ BiasAt operator+(int d) const { return BiasAt{s, off + d}; }
+};
+
 // Accumulator initialised with the bias of 32-row block r: lane group g holds
 // rows 8q + 4g + j (q, j = 0..3) in register 4q + j.
-__device__ __forceinline__ f32x16 bias_frag(const float* bias, int g) {
+__device__ __forceinline__ f32x16 bias_frag(BiasAt bias, int g) {
     f32x16 b;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-        const f32x4 v = *reinterpret_cast<const f32x4*>(bias + 8 * q + 4 * g);
+        const f32x4 v = *reinterpret_cast<const f32x4*>(bias.s + (bias.off + 8 * q + 4 * g));
         b[4 * q + 0] = v[0];
         b[4 * q + 1] = v[1];
         b[4 * q + 2] = v[2];
@@ -227,7 +237,7 @@ __device__ __forceinline__ f32x16 bias_frag(const float* bias, int g) {
 // steps.  BASE is the index of the pass's first fragment within its layer;
 // layers start on chunk boundaries, so chunk changes are known statically.
 template <int PR, int CB, int KS, int RBP, int BASE, class WS, class GetB, class Epi>
-__device__ __forceinline__ void run_pass(WS& st, int g, const float* bias, GetB& getB, Epi&& epi) {
+__device__ __forceinline__ void run_pass(WS& st, int g, BiasAt bias, GetB& getB, Epi&& epi) {
     using P = Prec<PR>;
     static_assert(P::U == 1, "heads run single-unit steps");
     constexpr int NF = KS * RBP;   // fragments of the pass, in (K step, row block) order
@@ -322,7 +332,7 @@ __device__ __forceinline__ void emit_fp8(const f32x16& a0, const f32x16& a1, u32
 // input; sa is the E8M0 scale of fp8 weights.  getB(k, c) returns the u32x4
 // k of the input (an fp8 step reads two).
 template <int OUT, int CB, int KS, int MP, class WS, class GetB, int NOUT>
-__device__ __forceinline__ void hidden_layer(WS& st, int g, const float* bias, GetB&& getB,
+__device__ __forceinline__ void hidden_layer(WS& st, int g, BiasAt bias, GetB&& getB,
                                              u32x4 (&out)[NOUT][CB], int sa = 127) {
     using M = Prec<MP>;
     constexpr int U = M::U;
@@ -694,7 +704,11 @@ __device__ __forceinline__ float one_minus_exp_neg(float x) {
 
 // ------------------------------------------------------------------ fused kernel
 
-constexpr int kBiasMax = 7 * 256 + 256 + 7 * 256 + 32;
+// LDS bias table: the seven depth layers, the seven shading layers and the
+// shading head (32 floats), then the depth head (B <= 256): every offset the
+// layer loops index is a compile-time constant.
+constexpr int kDepthHeadBias = 7 * 256 + 7 * 256 + 32;
+constexpr int kBiasMax = kDepthHeadBias + 256;
 
 // PR: network precision (layout.h Precision; an fp8 network keeps its first
 // layers and heads in bf16).  CB: 32-ray column blocks per wave.  NW: waves
@@ -819,7 +833,7 @@ render_kernel(const RenderArgs a) {
     auto g1 = [&](auto K, auto C) { return h1[CV(K)][CV(C)]; };
     // six 256 -> 256 ReLU layers whose biases start at bias_l0 and whose fp8
     // weight scales start at ws; the last one feeds a head in FP
-    auto hidden6 = [&](const float* bias_l0, const int32_t* ws) {
+    auto hidden6 = [&](BiasAt bias_l0, const int32_t* ws) {
         if constexpr (PR == kFP8) {
             for (int l = 0; l < 2; ++l) {
                 hidden_layer<kFP8, CB, KS_HID, kFP8>(st, g, bias_l0 + 256 * (2 * l), g0, h1, ws[2 * l]);
@@ -836,9 +850,9 @@ render_kernel(const RenderArgs a) {
     };
     {
         auto gin = [&](auto K, auto C) { return din[CV(K)][CV(C)]; };
-        hidden_layer<PR, CB, KS_D0, DIN == kDinEncoded ? FP : kF32>(st, g, bias_s, gin, h0);
+        hidden_layer<PR, CB, KS_D0, DIN == kDinEncoded ? FP : kF32>(st, g, BiasAt{bias_s, 0}, gin, h0);
     }
-    hidden6(bias_s + 256, a.wscale + 1);
+    hidden6(BiasAt{bias_s, 256}, a.wscale + 1);
     // Head of the depth network: B / 64 passes of 64 classes (32 * kRbPerPass).
     const int npass = a.B / (32 * kRbPerPass);
     constexpr int PASS_FRAGS = KS_H * kRbPerPass;
@@ -877,7 +891,8 @@ render_kernel(const RenderArgs a) {
                     }
                 } else {
                     run_pass<FP, CB, KS_H, kRbPerPass, q * PASS_FRAGS>(
-                        st, g, bias_s + 7 * 256 + 32 * kRbPerPass * p, g0, [&](auto R, auto C, const f32x16& acc) {
+                        st, g, BiasAt{bias_s, kDepthHeadBias + 32 * kRbPerPass * p}, g0,
+                        [&](auto R, auto C, const f32x16& acc) {
                             const int rowb = 32 * kRbPerPass * p + 32 * CV(R);   // + 4 g: rebase below
 #pragma unroll
                             for (int i = 0; i < 16; ++i) top[CV(C)].push(acc[i], rowb + 8 * (i / 4) + (i % 4));
@@ -901,7 +916,8 @@ render_kernel(const RenderArgs a) {
             constexpr int p = CV(PI);
             if (p < npass) {
                 run_pass<FP, CB, KS_H, kRbPerPass, p * PASS_FRAGS>(
-                    st, g, bias_s + 7 * 256 + 32 * kRbPerPass * p, g0, [&](auto R, auto C, const f32x16& acc) {
+                    st, g, BiasAt{bias_s, kDepthHeadBias + 32 * kRbPerPass * p}, g0,
+                    [&](auto R, auto C, const f32x16& acc) {
 #pragma unroll
                         for (int i = 0; i < 16; ++i) vals[CV(C)][p][CV(R)][i] = sigmoid<FP == kF32>(acc[i]);
                         dump_scores(p, CV(R), CV(C), acc);
@@ -936,7 +952,7 @@ render_kernel(const RenderArgs a) {
     };
 
     // ---- shading network per sample, composited front to back
-    const int s_bias = 7 * 256 + a.B;
+    const int s_bias = 7 * 256;
     float T[CB], Cr[CB], Cg[CB], Cb[CB], Dp[CB];
 #pragma unroll
     for (int cb = 0; cb < CB; ++cb) T[cb] = 1.0f, Cr[cb] = Cg[cb] = Cb[cb] = Dp[cb] = 0.0f;
@@ -960,15 +976,15 @@ render_kernel(const RenderArgs a) {
         }
         {
             auto gs = [&](auto K, auto C) { return sin_[CV(K)][CV(C)]; };
-            hidden_layer<PR, CB, KS_S0, FP>(st, g, bias_s + s_bias, gs, h0);
+            hidden_layer<PR, CB, KS_S0, FP>(st, g, BiasAt{bias_s, s_bias}, gs, h0);
         }
-        hidden6(bias_s + s_bias + 256, a.wscale + 9);
+        hidden6(BiasAt{bias_s, s_bias + 256}, a.wscale + 9);
         auto gh = [&](auto K, auto C) {
             if constexpr (CV(K) < KS_H) return h0[CV(K)][CV(C)];
             else return skip[CV(K) - KS_H][CV(C)];
         };
         run_pass<FP, CB, KS_H + KS_SK, 1, 0>(
-            st, g, bias_s + s_bias + 7 * 256, gh, [&](auto R, auto C, const f32x16& acc) {
+            st, g, BiasAt{bias_s, s_bias + 7 * 256}, gh, [&](auto R, auto C, const f32x16& acc) {
                 constexpr int cb = CV(C);
                 // lanes of group 0 hold rows 0..3 = (r, g, b, sigma) in registers 0..3
                 const float cr = sigmoid<FP == kF32>(acc[0]);
