@@ -124,6 +124,26 @@ def cpu_baseline(wl, weights, poses, n_sample):
                       f"os.cpu_count()={os.cpu_count()}"}
 
 
+def mfma_loop_ceiling(r, precision, stream, workgroups=2048):
+    """TFLOP/s of the library's register-fed MFMA loop in the workload's
+    precision (8 waves per SIMD, four independent chains each, random
+    operands), timed with events on the render stream after one warm-up."""
+    import torch
+    iters = {"bf16": 4096, "fp8": 2048, "fp32": 1024}[precision]
+    r.mfma_peak(workgroups, iters)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    flop = 0.0
+    for _ in range(5):
+        flop += r.mfma_peak(workgroups, iters)[1]
+    e1.record(stream)
+    torch.cuda.synchronize()
+    tflops = flop / (e0.elapsed_time(e1) * 1e-3) / 1e12
+    log(f"MFMA loop ceiling ({precision}): {tflops:.1f} TFLOP/s")
+    return tflops
+
+
 def bench_targets(args, tw):
     """Training targets (Sec. 5.1, Eq. 6-8) of the seeded depth maps: one
     step is one donerf_targets call over all P maps.  HBM-bound: each pixel
@@ -189,6 +209,8 @@ def main():
     ap.add_argument("--workload", default="frame400_n4_bf16")
     ap.add_argument("--cpu-sample", type=int, default=262144)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-mfma-loop", action="store_true",
+                    help="skip the register-fed MFMA loop that measures the matrix cores' ceiling")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (3 times), to calibrate the "
                          "FETCH_SIZE / WRITE_SIZE counters against known bytes")
@@ -252,6 +274,8 @@ def main():
     avg_kern_ms = float(np.mean(kern_ms))
     log(f"timed {args.steps} steps: wall {wall * 1e3:.2f} ms, kernel avg {avg_kern_ms:.4f} ms")
 
+    loop = mfma_loop_ceiling(r, wl.precision, stream) if not args.no_mfma_loop else None
+
     rays = wl.rays
     ms_step = wall * 1e3 / args.steps
     value = rays / (ms_step * 1e-3) / 1e6
@@ -295,6 +319,12 @@ def main():
                      "traffic": traffic,
                      "kernel": f"render_kernel<{wl.precision}>", "kernel_ms": round(avg_kern_ms, 4)},
     }
+    if loop is not None:
+        # the measured ceiling: a register-fed MFMA loop on random operands
+        line["roofline"]["mfma_loop"] = {"achieved": round(loop, 2), "frac_of_peak":
+                                         round(loop / MFMA_PEAK_TFLOPS[wl.precision], 4)}
+        if wl.precision != "fp8":   # the fp8 network mixes fp8 and bf16 layers
+            line["roofline"]["frac_of_mfma_loop"] = round(achieved / loop, 4)
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(wl, weights, poses, args.cpu_sample)
     r.close()

@@ -203,6 +203,24 @@ int donerf_debug_topn(donerf_t* h, const float* scores, int32_t rays, int32_t N,
                       int32_t* out_idx);
 
 /*
+ * Measured ceiling of the matrix cores, for the roofline of donerf_render:
+ * a register-fed MFMA loop in the handle's precision (BF16: 32 x 32 x 16
+ * bf16; FP8: 32 x 32 x 64 E4M3; FP32: 32 x 32 x 2 fp32), on the handle's
+ * stream.  workgroups x 4 waves each run four independent accumulator chains
+ * of `iters` steps on seeded random register operands drawn like the
+ * render's: A uniform in [-1, 1) like weights, B the positive part of such
+ * values like ReLU activations (no memory traffic, no dependence stalls).
+ *   workgroups  1..2^20 (a few per compute unit fill the device)
+ *   iters       1..2^24 steps per chain
+ *   sink        device, workgroups x 256 fp32, caller-owned: one sum of
+ *               accumulators per thread, written so the work is kept
+ *   flop        host, may be NULL: the launch's FLOP (2 per multiply-add)
+ * Time the launch with events on the handle's stream.
+ * Errors: E_INVALID_ARG (NULL handle or sink, sizes out of range), E_HIP.
+ */
+int donerf_debug_mfma_peak(donerf_t* h, int32_t workgroups, int32_t iters, float* sink, double* flop);
+
+/*
  * Training targets of the depth oracle (Sec. 5.1) for P depth maps, on the
  * handle's depth classes and stream:
  *   Eq. 6  C(z) = 1 for the class z with b_z <= d < b_{z+1} of the pixel's

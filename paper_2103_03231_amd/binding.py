@@ -38,7 +38,7 @@ MAX_SAMPLES = 16
 # Every function include/donerf.h declares.
 EXPORTS = ("donerf_weight_count", "donerf_create", "donerf_destroy", "donerf_set_stream",
            "donerf_render", "donerf_render_debug", "donerf_targets", "donerf_debug_topn",
-           "donerf_debug_bins", "donerf_status_str", "donerf_last_error")
+           "donerf_debug_bins", "donerf_debug_mfma_peak", "donerf_status_str", "donerf_last_error")
 
 
 class DonerfLibraryMissing(RuntimeError):
@@ -110,6 +110,8 @@ def lib():
         L.donerf_debug_topn.restype = ctypes.c_int
         L.donerf_debug_bins.argtypes = [vp, fp, fp, fp]
         L.donerf_debug_bins.restype = ctypes.c_int
+        L.donerf_debug_mfma_peak.argtypes = [vp, i32, i32, vp, ctypes.POINTER(ctypes.c_double)]
+        L.donerf_debug_mfma_peak.restype = ctypes.c_int
         L.donerf_status_str.argtypes, L.donerf_status_str.restype = [ctypes.c_int], ctypes.c_char_p
         L.donerf_last_error.argtypes, L.donerf_last_error.restype = [], ctypes.c_char_p
         _lib = L
@@ -178,6 +180,13 @@ def donerf_debug_topn(h, scores_ptr, rays, N, out_idx_ptr) -> None:
     _check(lib().donerf_debug_topn(h, scores_ptr, rays, N, out_idx_ptr))
 
 
+def donerf_debug_mfma_peak(h, workgroups, iters, sink_ptr) -> float:
+    """Enqueue the register-fed MFMA loop; returns the launch's FLOP."""
+    flop = ctypes.c_double(0.0)
+    _check(lib().donerf_debug_mfma_peak(h, workgroups, iters, sink_ptr, ctypes.byref(flop)))
+    return flop.value
+
+
 def donerf_debug_bins(h, n_bins):
     bounds = np.empty(n_bins + 1, np.float32)
     centres = np.empty(n_bins, np.float32)
@@ -217,6 +226,13 @@ class Renderer:
         out = t.empty((P, H, W, self.cfg.n_bins), dtype=t.float32, device=depth.device)
         donerf_targets(self.h, depth.data_ptr(), P, H, W, K, Z, out.data_ptr())
         return out
+
+    def mfma_peak(self, workgroups, iters):
+        """Enqueue the register-fed MFMA loop in the handle's precision;
+        returns (sink, FLOP of the launch)."""
+        import torch
+        sink = torch.empty(workgroups * 256, dtype=torch.float32, device="cuda")
+        return sink, donerf_debug_mfma_peak(self.h, workgroups, iters, sink.data_ptr())
 
     def alloc(self, P, H, W, N, depth=False, debug=False):
         t = self.torch

@@ -496,6 +496,18 @@ int donerf_debug_topn(donerf_t* h, const float* scores, int32_t rays, int32_t N,
     return DONERF_OK;
 }
 
+int donerf_debug_mfma_peak(donerf_t* h, int32_t workgroups, int32_t iters, float* sink, double* flop) {
+    g_err.clear();
+    if (!h) return fail(DONERF_E_INVALID_ARG, "handle is NULL");
+    if (!sink) return fail(DONERF_E_INVALID_ARG, "NULL buffer");
+    if (workgroups < 1 || workgroups > (1 << 20)) return fail(DONERF_E_INVALID_ARG, "workgroups must lie in [1, 2^20]");
+    if (iters < 1 || iters > (1 << 24)) return fail(DONERF_E_INVALID_ARG, "iters must lie in [1, 2^24]");
+    if (flop) *flop = (double)workgroups * 4 * 4 * (double)iters * mfma_step_flop(h->prec);
+    hipError_t e = launch_mfma_peak(h->prec, workgroups, iters, 0x5EED0u, sink, h->stream);
+    if (e != hipSuccess) return hip_fail(e, "mfma peak launch");
+    return DONERF_OK;
+}
+
 int donerf_targets(donerf_t* h, const float* depth, int32_t P, int32_t H, int32_t W, int32_t K, int32_t Z,
                    float* out) {
     g_err.clear();

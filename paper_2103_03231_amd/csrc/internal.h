@@ -82,6 +82,16 @@ hipError_t launch_softmax_rows(float* scores, uint32_t rows, int B, hipStream_t 
 hipError_t launch_topn(bool bf16_layout, int ncap, const float* scores, int32_t rays,
                        int32_t N, int32_t B, int32_t* out_idx, hipStream_t stream);
 
+// Register-fed MFMA loop (kernels.hip): workgroups x 4 waves, four
+// independent 32 x 32 chains of `iters` steps per wave in precision prec;
+// sink holds workgroups x 256 floats.
+hipError_t launch_mfma_peak(int prec, int workgroups, int iters, uint32_t seed, float* sink, hipStream_t stream);
+// FLOP of one chain step: a 32 x 32 x 16 bf16, 32 x 32 x 64 E4M3 or four
+// 32 x 32 x 2 fp32 MFMAs.
+constexpr double mfma_step_flop(int prec) {
+    return prec == kFP8 ? 2.0 * 32 * 32 * 64 : prec == kBF16 ? 2.0 * 32 * 32 * 16 : 2.0 * 32 * 32 * 8;
+}
+
 // Training targets (targets.hip): P depth maps of H x W, class bounds
 // bounds[0..B], window sizes K and Z (1..kTgtMaxK), out P x H x W x B.
 constexpr int kMaxBins = 256;

@@ -101,6 +101,94 @@ hipError_t launch_softmax_rows(float* scores, uint32_t rows, int B, hipStream_t 
     return hipGetLastError();
 }
 
+// ------------------------------------------------------------------ MFMA ceiling
+
+// lowbias32 (C. Wellons' integer hash): operand bits for the loop below.
+__device__ __forceinline__ uint32_t mix32(uint32_t x) {
+    x ^= x >> 16;
+    x *= 0x7feb352du;
+    x ^= x >> 15;
+    x *= 0x846ca68bu;
+    x ^= x >> 16;
+    return x;
+}
+
+// A uniform value in [-1, 1) and the next hash state.
+__device__ __forceinline__ float rand_unit(uint32_t& st) {
+    st = mix32(st + 0x9e3779b9u);
+    return (float)(int32_t)st * 0x1p-31f;
+}
+
+// One u32x4 operand unit of random values in the precision's element format:
+// uniform in [-1, 1) like the weights, or (RELU) their positive part like
+// the activations a ReLU layer passes on, half of them zero.
+template <int PR, bool RELU>
+__device__ __forceinline__ u32x4 rand_operand(uint32_t& st) {
+    auto next = [&]() { const float x = rand_unit(st); return RELU ? fmaxf(x, 0.0f) : x; };
+    u32x4 v;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+        if constexpr (PR == kBF16) {
+            const float x = next(), y = next();
+            v[w] = pack_bf16x2(x, y);
+        } else if constexpr (PR == kFP8) {
+            const float x0 = next(), x1 = next(), x2 = next(), x3 = next();
+            uint32_t q = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(x0, x1, 0, false);
+            v[w] = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(x2, x3, (int)q, true);
+        } else {
+            v[w] = __float_as_uint(next());
+        }
+    }
+    return v;
+}
+
+// Register-fed MFMA loop: each wave runs four independent 32 x 32
+// accumulator chains of `iters` steps on register operands drawn like the
+// render kernel's (uniform weights as A, ReLU activations as B), so the
+// matrix pipes never wait on memory or on a dependence.  What it sustains
+// (the operands' data-dependent power included) is the practical ceiling of
+// the render kernel's MFMA stream.  One value per thread keeps the work live.
+template <int PR>
+__global__ __launch_bounds__(256) void mfma_peak_kernel(int iters, uint32_t seed, float* sink) {
+    using P = Prec<PR>;
+    constexpr int U = PR == kFP8 ? 2 : 1;
+    const uint32_t t = blockIdx.x * 256u + threadIdx.x;
+    uint32_t st = mix32(seed ^ mix32(t));
+    u32x4 a[2][U], b[2][U];
+#pragma unroll
+    for (int m = 0; m < 2; ++m)
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            a[m][u] = rand_operand<PR, false>(st);
+            b[m][u] = rand_operand<PR, true>(st);
+        }
+    f32x16 acc[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[c][e] = 0.0f;
+    for (int i = 0; i < iters; ++i) {
+        acc[0] = P::mma(a[0], b[0], acc[0], 127);
+        acc[1] = P::mma(a[1], b[0], acc[1], 127);
+        acc[2] = P::mma(a[0], b[1], acc[2], 127);
+        acc[3] = P::mma(a[1], b[1], acc[3], 127);
+    }
+    float s = 0.0f;
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) s += acc[c][e];
+    sink[t] = s;
+}
+
+hipError_t launch_mfma_peak(int prec, int workgroups, int iters, uint32_t seed, float* sink, hipStream_t stream) {
+    const dim3 grid(workgroups), block(256);
+    if (prec == kFP8) hipLaunchKernelGGL(mfma_peak_kernel<kFP8>, grid, block, 0, stream, iters, seed, sink);
+    else if (prec == kBF16) hipLaunchKernelGGL(mfma_peak_kernel<kBF16>, grid, block, 0, stream, iters, seed, sink);
+    else hipLaunchKernelGGL(mfma_peak_kernel<kF32>, grid, block, 0, stream, iters, seed, sink);
+    return hipGetLastError();
+}
+
 hipError_t launch_topn(bool bf16_layout, int ncap, const float* scores, int32_t rays, int32_t N,
                        int32_t B, int32_t* out_idx, hipStream_t stream) {
     const int cb = bf16_layout ? 2 : 1;

@@ -93,6 +93,7 @@ def test_calls_on_null_handle():
                lambda: b.donerf_debug_topn(None, 1, 4, 4, 1),
                lambda: b.donerf_targets(None, 1, 1, 4, 4, 5, 5, 1),
                lambda: b.donerf_debug_bins(None, 128),
+               lambda: b.donerf_debug_mfma_peak(None, 1, 1, 1),
                lambda: b.donerf_set_stream(None, 0)):
         with pytest.raises(b.DonerfError) as e:
             fn()
