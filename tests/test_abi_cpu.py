@@ -108,3 +108,23 @@ def test_create_without_gpu_reports_device_error():
     with pytest.raises(b.DonerfError) as e:
         b.donerf_create(b.Config(), W128)
     assert e.value.status == b.E_DEVICE
+
+
+def test_missing_library_fails_loudly():
+    """Without the built library every entry point raises; nothing falls
+    back to another implementation.  Run in a fresh interpreter, since the
+    module keeps the library it loaded."""
+    import subprocess
+    import sys
+    code = ("from paper_2103_03231_amd import binding as b, inputs\n"
+            "b.LIB_PATH = '/nonexistent/libdonerf.so'\n"
+            "for f in (lambda: b.donerf_weight_count(128),\n"
+            "          lambda: b.Renderer(b.Config(n_bins=128, n_max=4), inputs.make_weights(128, 0))):\n"
+            "    try:\n"
+            "        f()\n"
+            "    except b.DonerfLibraryMissing:\n"
+            "        continue\n"
+            "    raise SystemExit('no error')\n"
+            "print('raised')\n")
+    r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0 and "raised" in r.stdout, r.stderr[-2000:]
