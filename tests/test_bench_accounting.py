@@ -1,0 +1,56 @@
+"""The bench's work accounting on the CPU: the algorithmic FLOP per ray it
+divides by the kernel time equals twice the multiply-adds of the networks
+the oracle parses out of a weight blob (each layer's W is out x in), the
+padded count only adds tile padding, and the fp8 share is the twelve hidden
+layers.  (The oracle's own count is pinned to Table 2's MFLOP per pixel in
+test_oracle_pins.)"""
+import pytest
+
+import bench
+from oracle import donerf_oracle as O
+from paper_2103_03231_amd import inputs
+
+
+def _macs_from_blob(n_bins, N, depth_input="encoded"):
+    d_layers, s_layers = O.split_weights(inputs.make_weights(n_bins, 0, depth_input), n_bins, depth_input)
+    macs = lambda layers: sum(W.shape[0] * W.shape[1] for W, _ in layers)
+    return macs(d_layers) + N * macs(s_layers)
+
+
+@pytest.mark.parametrize("n_bins", [64, 128, 256])
+@pytest.mark.parametrize("N", [1, 2, 4, 8, 16])
+def test_algorithmic_flop_is_twice_the_parsed_macs(n_bins, N):
+    assert bench.algorithmic_flop_per_ray(N, n_bins) == 2 * _macs_from_blob(n_bins, N)
+    assert bench.algorithmic_flop_per_ray(N, n_bins) == 2 * O.mlp_macs_per_ray(N, n_bins)
+
+
+def test_headline_figures():
+    # 5 x 400 x 400 rays, N = 4, B = 128: 4,181,856 FLOP per ray, 3.345 TFLOP per step
+    assert bench.algorithmic_flop_per_ray(4, 128) == 4_181_856
+    assert bench.algorithmic_flop_per_ray(4, 128) * 800_000 == 3_345_484_800_000
+
+
+@pytest.mark.parametrize("N", [1, 4, 16])
+def test_padding_only_adds(N):
+    alg, pad = bench.algorithmic_flop_per_ray(N, 128), bench.padded_flop_per_ray(N, 128)
+    # K padding 90 -> 96 and 63 -> 64 and 283 -> 288, shading head 4 -> 32 rows
+    assert pad - alg == 2 * ((96 - 90) * 256 + N * ((64 - 63) * 256 + 288 * 32 - 283 * 4))
+
+
+def test_fp8_share_and_mixed_peak():
+    N = 4
+    tot, f8 = bench.algorithmic_flop_per_ray(N, 128), bench.fp8_flop_per_ray(N)
+    assert f8 == 2 * 6 * 256 * 256 * (1 + N)
+    peak = bench.mixed_peak(N, 128, 90)
+    assert bench.MFMA_PEAK_TFLOPS["bf16"] < peak < bench.MFMA_PEAK_TFLOPS["fp8"]
+    # the time of the whole at the mixed peak is the sum of the parts' times
+    t_parts = f8 / bench.MFMA_PEAK_TFLOPS["fp8"] + (tot - f8) / bench.MFMA_PEAK_TFLOPS["bf16"]
+    assert abs(tot / peak - t_parts) < 1e-9 * t_parts
+
+
+def test_positions_input_folds_to_nine_columns():
+    # the paper's unencoded input (6 + 3 B values) is affine in the ray, so the
+    # first layer runs as 9 columns; the parsed network itself has 6 + 3 B
+    assert bench.depth_in_folded("positions") == 9
+    d_layers, _ = O.split_weights(inputs.make_weights(128, 0, "positions"), 128, "positions")
+    assert d_layers[0][0].shape == (256, 6 + 3 * 128)
