@@ -170,6 +170,12 @@ int donerf_set_stream(donerf_t* h, void* stream);
  *              or NULL to skip
  * The work is enqueued on the handle's stream; results are valid once the
  * stream has been synchronised.  No allocation, no host synchronisation.
+ * The call issues kernel launches only (the poses travel in the launch
+ * arguments; no memset or copy), so it can be captured into a HIP graph on
+ * the handle's stream and replayed; a replay renders the poses, sizes and
+ * buffers of the captured call.  Calls on one handle share its scratch
+ * buffer for the split tail: do not let two of them overlap on different
+ * streams.
  * Errors: E_INVALID_ARG (NULL handle/poses/out_rgb, P, H, W < 1, N out of
  * range, P*H*W >= 2^31, H*W > 2^24), E_NONFINITE (pose), E_HIP (launch
  * failed).
