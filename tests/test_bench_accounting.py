@@ -54,3 +54,18 @@ def test_positions_input_folds_to_nine_columns():
     assert bench.depth_in_folded("positions") == 9
     d_layers, _ = O.split_weights(inputs.make_weights(128, 0, "positions"), 128, "positions")
     assert d_layers[0][0].shape == (256, 6 + 3 * 128)
+
+
+def test_more_than_one_gpu_exits_with_a_message():
+    """The rays of a frame are independent; this library measures one GPU's
+    share, and asking for several exits before any device work."""
+    import json
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"], cwd=root,
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    msg = json.loads(r.stdout.strip().splitlines()[-1])
+    assert "one GPU" in msg["error"]
