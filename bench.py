@@ -317,7 +317,8 @@ def main():
                      **({"peak_note": "fp8 hidden layers at 5000, bf16 first layers and heads at 2500, "
                                       "combined by their share of the work"} if wl.precision == "fp8" else {}),
                      "traffic": traffic,
-                     "kernel": f"render_kernel<{wl.precision}>", "kernel_ms": round(avg_kern_ms, 4)},
+                     "kernel": f"render_kernel<{wl.precision}>", "kernel_ms": round(avg_kern_ms, 4),
+                     "kernel_ms_median": round(float(np.median(kern_ms)), 4)},
     }
     if loop is not None:
         # the measured ceiling: a register-fed MFMA loop on random operands
