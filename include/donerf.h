@@ -184,6 +184,26 @@ int donerf_render(donerf_t* h, const float* cam_poses, int32_t P, int32_t H, int
                   int32_t N, float* out_rgb, float* out_depth);
 
 /*
+ * donerf_render for callers that cannot allocate device memory at all (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same kernels and results, with the split tail's partial
+ * results kept in a static device array of the library instead of the
+ * handle's buffer.  The array holds 5 x 256 x 256 floats (1.25 MiB) on every
+ * device the library runs on, until the process ends; its address is looked
+ * up when a handle is created, so this call makes no HIP call other than its
+ * kernel launches and allocates nothing.  Every call on one device shares that
+ * device's array (no contents need clearing: each launch writes every part it
+ * reads back), so calls that overlap on one device, on any handles or
+ * streams, race and must not be issued.
+ * Arguments and errors as donerf_render, plus E_UNSUPPORTED when a launch's
+ * split tail needs more than the array holds (only on devices with more than
+ * 256 compute units) and E_HIP when the array's address could not be looked
+ * up at create.
+ */
+int donerf_render_static_scratch(donerf_t* h, const float* cam_poses, int32_t P, int32_t H, int32_t W,
+                                 int32_t N, float* out_rgb, float* out_depth);
+
+/*
  * donerf_render with optional per-ray intermediate outputs, for testing.
  *   out_bins     device, P x H x W x N int32: the class of each sample in sample
  *                (= depth) order, or NULL

@@ -37,8 +37,9 @@ MAX_SAMPLES = 16
 
 # Every function include/donerf.h declares.
 EXPORTS = ("donerf_weight_count", "donerf_create", "donerf_destroy", "donerf_set_stream",
-           "donerf_render", "donerf_render_debug", "donerf_targets", "donerf_debug_topn",
-           "donerf_debug_bins", "donerf_debug_mfma_peak", "donerf_status_str", "donerf_last_error")
+           "donerf_render", "donerf_render_static_scratch", "donerf_render_debug", "donerf_targets",
+           "donerf_debug_topn", "donerf_debug_bins", "donerf_debug_mfma_peak", "donerf_status_str",
+           "donerf_last_error")
 
 
 class DonerfLibraryMissing(RuntimeError):
@@ -102,6 +103,8 @@ def lib():
         L.donerf_set_stream.argtypes, L.donerf_set_stream.restype = [vp, vp], ctypes.c_int
         L.donerf_render.argtypes = [vp, fp, i32, i32, i32, i32, vp, vp]
         L.donerf_render.restype = ctypes.c_int
+        L.donerf_render_static_scratch.argtypes = [vp, fp, i32, i32, i32, i32, vp, vp]
+        L.donerf_render_static_scratch.restype = ctypes.c_int
         L.donerf_render_debug.argtypes = [vp, fp, i32, i32, i32, i32, vp, vp, vp, vp, vp]
         L.donerf_render_debug.restype = ctypes.c_int
         L.donerf_targets.argtypes = [vp, vp, i32, i32, i32, i32, i32, vp]
@@ -163,6 +166,11 @@ def _poses(poses):
 def donerf_render(h, poses, P, H, W, N, out_rgb_ptr, out_depth_ptr=None) -> None:
     p = _poses(poses)
     _check(lib().donerf_render(h, _fptr(p), P, H, W, N, out_rgb_ptr, out_depth_ptr))
+
+
+def donerf_render_static_scratch(h, poses, P, H, W, N, out_rgb_ptr, out_depth_ptr=None) -> None:
+    p = _poses(poses)
+    _check(lib().donerf_render_static_scratch(h, _fptr(p), P, H, W, N, out_rgb_ptr, out_depth_ptr))
 
 
 def donerf_render_debug(h, poses, P, H, W, N, out_rgb_ptr, out_depth_ptr=None,

@@ -26,6 +26,8 @@ struct donerf_handle {
     int n_d_chunks, n_s_chunks, bias_len;
     int n_cu;            // compute units: workgroups of one full round
     float* partial;      // device: split-tail parts, n_cu * 256 rays * 5 floats
+    float* static_scratch;         // device address of the static scratch (kernels.hip)
+    hipError_t static_scratch_err; // why it could not be looked up, if it is NULL
     std::vector<float> h_bounds, h_centres, h_widths;
 };
 
@@ -280,10 +282,49 @@ int validate_render(const donerf_t* h, const float* poses, int32_t P, int32_t H,
 
 int ncap_for(int N) { return N <= 4 ? 4 : N <= 8 ? 8 : 16; }
 
+// Split of the last, partial round of tiles: n_full tiles run whole, the
+// remaining rem tiles are each split `split` ways by samples.
+struct TailPlan {
+    uint32_t n_full, rem, split;
+};
+
+TailPlan plan_tail(const donerf_t* h, uint32_t total_rays, int32_t N) {
+    // Full rounds of one workgroup per CU run as they are.  The tiles of a
+    // last, partial round are split by samples over up to n_cu / r
+    // workgroups each (every part recomputes the depth network), and a
+    // combine pass composites the parts.
+    const uint32_t rpb = (uint32_t)rays_per_block(h->prec);
+    const uint32_t tiles = (total_rays + rpb - 1) / rpb;
+    const uint32_t round = (uint32_t)h->n_cu;
+    const uint32_t full = tiles / round * round, rem = tiles - full;
+    uint32_t split = rem ? round / rem : 1;
+    if (split > (uint32_t)N) split = (uint32_t)N;
+    if (split < 1) split = 1;
+    return TailPlan{split > 1 ? full : tiles, split > 1 ? rem : 0, split};
+}
+
+// Floats of split-tail scratch a plan writes: 5 per ray and part.
+size_t tail_floats(const donerf_t* h, const TailPlan& t) {
+    return t.split > 1 ? (size_t)5 * t.rem * (size_t)rays_per_block(h->prec) * t.split : 0;
+}
+
+// partial: split-tail scratch of partial_cap floats (the handle's buffer, or
+// the static scratch).
 int render_impl(donerf_t* h, const float* poses, int32_t P, int32_t H, int32_t W, int32_t N, float* out_rgb,
-                float* out_depth, int32_t* out_bins, float* out_scores, float* out_samples) {
+                float* out_depth, int32_t* out_bins, float* out_scores, float* out_samples, float* partial,
+                size_t partial_cap) {
     int rc = validate_render(h, poses, P, H, W, N, out_rgb);
     if (rc) return rc;
+    const size_t hw = (size_t)H * W;
+    // every launch's scratch need is known before the first one is enqueued
+    for (int32_t p0 = 0; p0 < P; p0 += kMaxPosesPerLaunch) {
+        const int np = P - p0 < kMaxPosesPerLaunch ? P - p0 : kMaxPosesPerLaunch;
+        const size_t need = tail_floats(h, plan_tail(h, (uint32_t)(np * hw), N));
+        if (need > partial_cap)
+            return fail(DONERF_E_UNSUPPORTED, "the split tail needs " + std::to_string(need) +
+                                                  " floats of scratch, " + std::to_string(partial_cap) +
+                                                  " are available");
+    }
     const donerf_cfg& c = h->cfg;
     RenderArgs a;
     std::memset(&a, 0, sizeof a);
@@ -309,7 +350,6 @@ int render_impl(donerf_t* h, const float* poses, int32_t P, int32_t H, int32_t W
     a.dmax = c.far_dist;
     a.log2_span1 = (float)std::log2((double)c.far_dist - (double)c.near_dist + 1.0);
     const int place = c.select == DONERF_SELECT_CDF ? 1 : 0;
-    const size_t hw = (size_t)H * W;
     for (int32_t p0 = 0; p0 < P; p0 += kMaxPosesPerLaunch) {
         const int np = P - p0 < kMaxPosesPerLaunch ? P - p0 : kMaxPosesPerLaunch;
         a.n_poses = np;
@@ -320,26 +360,16 @@ int render_impl(donerf_t* h, const float* poses, int32_t P, int32_t H, int32_t W
         a.out_bins = out_bins ? out_bins + (size_t)p0 * hw * N : nullptr;
         a.out_scores = out_scores ? out_scores + (size_t)p0 * hw * c.n_bins : nullptr;
         a.out_samples = out_samples ? out_samples + (size_t)p0 * hw * N * 2 : nullptr;
-        // Full rounds of one workgroup per CU run as they are.  The tiles of a
-        // last, partial round are split by samples over up to n_cu / r
-        // workgroups each (every part recomputes the depth network), and a
-        // combine pass composites the parts.
-        const uint32_t rpb = (uint32_t)rays_per_block(h->prec);
-        const uint32_t tiles = (a.total_rays + rpb - 1) / rpb;
-        const uint32_t round = (uint32_t)h->n_cu;
-        const uint32_t full = tiles / round * round, rem = tiles - full;
-        uint32_t split = rem ? round / rem : 1;
-        if (split > (uint32_t)N) split = (uint32_t)N;
-        if (split < 1) split = 1;
-        a.n_full = split > 1 ? full : tiles;
-        a.split = (int32_t)split;
-        a.partial = h->partial;
+        const TailPlan tp = plan_tail(h, a.total_rays, N);
+        a.n_full = tp.n_full;
+        a.split = (int32_t)tp.split;
+        a.partial = partial;
         std::memcpy(a.wscale, h->wscale, sizeof a.wscale);
         hipError_t e = launch_render(h->prec, ncap_for(N), place,
                                      c.depth_input == DONERF_DEPTH_POSITIONS ? kDinPositions : kDinEncoded, a,
-                                     split > 1 ? rem : 0, h->stream);
+                                     tp.rem, h->stream);
         if (e != hipSuccess) return hip_fail(e, "render launch");
-        if (split > 1) {
+        if (tp.split > 1) {
             e = launch_combine(h->prec, a, h->stream);
             if (e != hipSuccess) return hip_fail(e, "combine launch");
         }
@@ -447,6 +477,14 @@ int donerf_create(const donerf_cfg* cfg, const float* weights, size_t n_weights,
         donerf_destroy(h);
         return fail(DONERF_E_NOMEM, std::string("hipMalloc: ") + hipGetErrorString(e));
     }
+    // the static scratch of donerf_render_static_scratch, looked up here
+    // (with the handle's device current) so that entry point makes no HIP
+    // call besides its launches; a failure surfaces there
+    h->static_scratch_err = static_scratch_address(dev, &h->static_scratch);
+    if (h->static_scratch_err != hipSuccess) {
+        (void)hipGetLastError();
+        h->static_scratch = nullptr;
+    }
     if ((e = hipMemcpy(h->d_frags, frags.data(), frags.size(), hipMemcpyHostToDevice)) != hipSuccess ||
         (e = hipMemcpy(h->bias, bias.data(), sizeof(float) * bias.size(), hipMemcpyHostToDevice)) != hipSuccess ||
         (e = hipMemcpy(h->bins, bins.data(), sizeof(float) * bins.size(), hipMemcpyHostToDevice)) != hipSuccess) {
@@ -475,14 +513,25 @@ int donerf_set_stream(donerf_t* h, void* stream) {
 int donerf_render(donerf_t* h, const float* cam_poses, int32_t P, int32_t H, int32_t W, int32_t N,
                   float* out_rgb, float* out_depth) {
     g_err.clear();
-    return render_impl(h, cam_poses, P, H, W, N, out_rgb, out_depth, nullptr, nullptr, nullptr);
+    return render_impl(h, cam_poses, P, H, W, N, out_rgb, out_depth, nullptr, nullptr, nullptr,
+                       h ? h->partial : nullptr, h ? (size_t)5 * 256 * (size_t)h->n_cu : 0);
+}
+
+int donerf_render_static_scratch(donerf_t* h, const float* cam_poses, int32_t P, int32_t H, int32_t W,
+                                 int32_t N, float* out_rgb, float* out_depth) {
+    g_err.clear();
+    if (h && !h->static_scratch)
+        return hip_fail(h->static_scratch_err, "static scratch lookup at create");
+    return render_impl(h, cam_poses, P, H, W, N, out_rgb, out_depth, nullptr, nullptr, nullptr,
+                       h ? h->static_scratch : nullptr, kStaticScratchFloats);
 }
 
 int donerf_render_debug(donerf_t* h, const float* cam_poses, int32_t P, int32_t H, int32_t W, int32_t N,
                         float* out_rgb, float* out_depth, int32_t* out_bins, float* out_scores,
                         float* out_samples) {
     g_err.clear();
-    return render_impl(h, cam_poses, P, H, W, N, out_rgb, out_depth, out_bins, out_scores, out_samples);
+    return render_impl(h, cam_poses, P, H, W, N, out_rgb, out_depth, out_bins, out_scores, out_samples,
+                       h ? h->partial : nullptr, h ? (size_t)5 * 256 * (size_t)h->n_cu : 0);
 }
 
 int donerf_debug_topn(donerf_t* h, const float* scores, int32_t rays, int32_t N, int32_t* out_idx) {

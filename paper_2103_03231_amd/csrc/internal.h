@@ -78,6 +78,14 @@ hipError_t launch_render_fp8_cdf(int ncap, int din, const RenderArgs& a, dim3 gr
 // Composites the split parts of rays [n_full * rays_per_block, total_rays)
 // into out_rgb / out_depth.
 hipError_t launch_combine(int prec, const RenderArgs& a, hipStream_t stream);
+// Floats of the static device scratch behind donerf_render_static_scratch:
+// the split tail's parts (5 floats per ray and part) of up to 256 compute
+// units x 256 rays, 1.25 MiB per device.
+constexpr size_t kStaticScratchFloats = (size_t)5 * 256 * 256;
+constexpr int kMaxDevices = 64;
+// Device address of that scratch on `device`, which must be the current
+// device; looked up once per device, then cached.
+hipError_t static_scratch_address(int device, float** out);
 hipError_t launch_softmax_rows(float* scores, uint32_t rows, int B, hipStream_t stream);
 hipError_t launch_topn(bool bf16_layout, int ncap, const float* scores, int32_t rays,
                        int32_t N, int32_t B, int32_t* out_idx, hipStream_t stream);

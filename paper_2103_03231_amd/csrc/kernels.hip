@@ -1,6 +1,9 @@
 // kernels.hip - the small kernels around the fused render kernel (split-tail
-// combine, softmax of dumped scores, stand-alone top-N for testing) and the
-// dispatch of render launches to the per-variant translation units.
+// combine, softmax of dumped scores, stand-alone top-N for testing), the
+// static scratch of the allocation-free render, and the dispatch of render
+// launches to the per-variant translation units.
+#include <mutex>
+
 #include "render_kernel.h"
 
 namespace donerf {
@@ -86,6 +89,30 @@ hipError_t launch_render(int prec, int ncap, int place, int din, const RenderArg
                                   : launch_render_bf16_topn(ncap, din, a, grid, stream);
     return place == kPlaceCdf ? launch_render_fp32_cdf(ncap, din, a, grid, stream)
                               : launch_render_fp32_topn(ncap, din, a, grid, stream);
+}
+
+// ------------------------------------------------------------------ static scratch
+
+// The split tail's partial results of donerf_render_static_scratch: a
+// file-scope device array, so that entry point allocates nothing.  Each
+// device holds its own copy, at its own address, until the process ends.
+static __device__ __align__(256) float scratch[kStaticScratchFloats];
+
+hipError_t static_scratch_address(int device, float** out) {
+    static std::mutex mu;
+    static float* ptr[kMaxDevices] = {};
+    if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!ptr[device]) {
+        // the array's name is a host-side stand-in; kernels need the
+        // device address, which this call returns for the current device
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        ptr[device] = static_cast<float*>(p);
+    }
+    *out = ptr[device];
+    return hipSuccess;
 }
 
 hipError_t launch_combine(int prec, const RenderArgs& a, hipStream_t stream) {

@@ -89,6 +89,7 @@ def test_create_rejects_bad_weights():
 def test_calls_on_null_handle():
     poses = inputs.make_poses([0])
     for fn in (lambda: b.donerf_render(None, poses, 1, 4, 4, 4, 1),
+               lambda: b.donerf_render_static_scratch(None, poses, 1, 4, 4, 4, 1),
                lambda: b.donerf_render_debug(None, poses, 1, 4, 4, 4, 1),
                lambda: b.donerf_debug_topn(None, 1, 4, 4, 1),
                lambda: b.donerf_targets(None, 1, 1, 4, 4, 5, 5, 1),
