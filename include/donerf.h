@@ -70,9 +70,14 @@ typedef enum donerf_select {
     DONERF_SELECT_TOPN = 0,         /* one sample at the centre of each of the N
                                        highest-scoring classes; its width is
                                        the class width                          */
-    DONERF_SELECT_TOPN_SOFTMAX = 1, /* the same classes, ranked on the softmax
-                                       of the scores (strictly monotone, so the
-                                       selection equals DONERF_SELECT_TOPN)     */
+    DONERF_SELECT_TOPN_SOFTMAX = 1, /* the scores filtered by a softmax: the
+                                       selection ranks the raw scores exactly
+                                       as DONERF_SELECT_TOPN (the softmax is
+                                       monotone; in fp32 it can also map
+                                       distinct scores to equal values, so it
+                                       is not ranked itself); the softmax only
+                                       transforms the scores a debug render
+                                       dumps                                   */
     DONERF_SELECT_CDF = 2           /* Sec. 5.1, Fig. 7: the class values
                                        sigmoid(score) as a piecewise-constant
                                        PDF over the classes (uniform in the

@@ -256,27 +256,119 @@ def split_weights(blob, n_bins, depth_input="encoded"):
     return layers[:8], layers[8:]
 
 
-def mlp(layers, x, precision="fp64", skip=None, round_input=True):
+def activation(y, rounding):
+    """A hidden unit's output: ReLU of its pre-activation y, then the rounding
+    point of the network ('bf16', 'e4m3' with the clamp at 448 the E4M3 range
+    imposes, or 'none'); rounding None is a head's output, y itself.
+    Monotone non-decreasing in y."""
+    if rounding is None:
+        return np.asarray(y, dtype=np.float64)
+    r = np.maximum(y, 0.0)
+    if rounding == "bf16":
+        return round_bf16(r)
+    if rounding == "e4m3":
+        return round_e4m3(np.minimum(r, E4M3_MAX))
+    return r
+
+
+def layer_arithmetic(precision, li, n):
+    """How layer li of an n-layer network of the given precision computes:
+    (weights as the layer uses them, the arithmetic of its products - 'fp64',
+    'bf16' or 'fp8' - and the rounding of its output for ``activation``).
+    bf16: bf16 weights, outputs rounded to bf16.  fp8 (``mlp_fp8``): bf16
+    first and last layers, fp8 weights elsewhere, outputs rounded to E4M3
+    except the one the last layer reads (bf16).  The last layer's output is a
+    head (no ReLU, no rounding)."""
+    last = li == n - 1
+    if precision == "fp8":
+        bf16_layer = li in (0, n - 1)
+        wq = round_bf16 if bf16_layer else quantize_fp8_weights
+        kind = "bf16" if bf16_layer else "fp8"
+        out = None if last else "bf16" if li == n - 2 else "e4m3"
+    elif precision == "bf16":
+        wq, kind, out = round_bf16, "bf16", (None if last else "bf16")
+    else:
+        wq, kind, out = (lambda a: np.asarray(a, dtype=np.float64)), "fp64", (None if last else "none")
+    return wq, kind, out
+
+
+def _jittered(y, h, Wq, b, kind, jitter):
+    """y moved by an accumulation error the evaluation may make (see
+    ``mlp``); y itself without jitter."""
+    if jitter is None:
+        return y
+    rng, rho = jitter
+    beta = accumulation_bound(h, Wq, b)
+    return y + rho[kind] * beta * rng.uniform(-1.0, 1.0, size=y.shape)
+
+
+def _jittered_input(x, jitter):
+    """Encoded features moved by up to rho['input'] (absolute) before they are
+    rounded: an evaluation of sine and cosine within that error (see ``mlp``)."""
+    x = np.asarray(x, dtype=np.float64)
+    if jitter is None or not jitter[1].get("input"):
+        return x
+    rng, rho = jitter
+    return x + rho["input"] * rng.uniform(-1.0, 1.0, size=x.shape)
+
+
+def mlp(layers, x, precision="fp64", skip=None, round_input=True, jitter=None, trace=None):
     """ReLU MLP: h = ReLU(W_l h + b_l) for every layer but the last, whose
     output is returned without activation.  ``skip`` (rows x s) is appended to
     the last layer's input (App. D's single direction skip).  x is (rows, in).
     In bf16 mode weights, inputs (unless ``round_input`` is false) and hidden
-    activations are rounded to bf16; sums accumulate in fp64.  fp8 mode:
-    ``mlp_fp8``."""
-    if precision == "fp8":
-        return mlp_fp8(layers, x, skip, round_input)
-    rb = round_bf16 if precision == "bf16" else (lambda a: np.asarray(a, dtype=np.float64))
-    h = rb(x) if round_input else np.asarray(x, dtype=np.float64)
+    activations are rounded to bf16; sums accumulate in fp64.  fp8 mode: the
+    mixed network of ``mlp_fp8``.  Each layer computes as
+    ``layer_arithmetic`` states.
+
+    Checking aids, not part of the method: ``jitter = (rng, rho)`` moves every
+    pre-activation by a uniform amount within rho[kind] times its
+    ``accumulation_bound`` before the activation is taken (kind: 'fp64',
+    'bf16' or 'fp8', the arithmetic of the layer's products), i.e. evaluates
+    the network as an implementation whose sums carry that much error may;
+    rho['input'] (optional) moves the rounded inputs (encoded features and
+    the skip) by up to that absolute amount first, as an encoding whose sine
+    and cosine carry that error may; ``trace`` (a list) receives (input,
+    weights as used, bias, pre-activation, rounding of the output) per
+    layer."""
+    rb = round_bf16 if precision in ("bf16", "fp8") else (lambda a: np.asarray(a, dtype=np.float64))
+    h = rb(_jittered_input(x, jitter)) if round_input else np.asarray(x, dtype=np.float64)
     n = len(layers)
     for li, (W, b) in enumerate(layers):
         if li == n - 1 and skip is not None:
-            h = np.concatenate([h, rb(skip)], axis=1)
-        y = h @ rb(W).T + b
-        if li < n - 1:
-            h = rb(np.maximum(y, 0.0))
-        else:
-            h = y
+            h = np.concatenate([h, rb(_jittered_input(skip, jitter))], axis=1)
+        wq, kind, out_round = layer_arithmetic(precision, li, n)
+        Wq = wq(W)
+        y = _jittered(h @ Wq.T + b, h, Wq, b, kind, jitter)
+        if trace is not None:
+            trace.append((h, Wq, b, y, out_round))
+        h = activation(y, out_round)
     return h
+
+
+def mlp_fp8(layers, x, skip=None, round_input=True, jitter=None, trace=None):
+    """The mixed fp8 network.  The paper leaves lower bit widths as future
+    headroom (Sec. 6.1) and fixes no scheme; this one keeps the first and the
+    last layer in bf16 (weights, inputs and skip rounded to bf16) and runs
+    the hidden layers in fp8: weights by ``quantize_fp8_weights``, inputs in
+    E4M3.  Each activation after bias and ReLU is clamped to 448 and rounded
+    to E4M3 where an fp8 layer reads it; where the last layer reads it, it is
+    rounded to bf16 (no clamp).  Sums accumulate in fp64.  ``jitter`` and
+    ``trace`` as in ``mlp``."""
+    return mlp(layers, x, "fp8", skip, round_input, jitter, trace)
+
+
+def layer_preactivation(layers, li, h, precision):
+    """Layer li of a network evaluated on a given input h (rows, in), as
+    ``mlp`` evaluates it: returns the exact pre-activations (fp64), their
+    ``accumulation_bound`` and the rounding of the layer's output.  A
+    checking aid: it lets a test feed each layer the GPU's own output of the
+    layer before ("teacher forcing")."""
+    W, b = layers[li]
+    wq, _, out_round = layer_arithmetic(precision, li, len(layers))
+    Wq = wq(W)
+    h = np.asarray(h, dtype=np.float64)
+    return h @ Wq.T + b, accumulation_bound(h, Wq, b), out_round
 
 
 def depth_positions_input(o, r, ou, centre, d_max, centres):
@@ -296,27 +388,32 @@ def depth_positions_input(o, r, ou, centre, d_max, centres):
     return np.concatenate([v, r.astype(F32), p.reshape(o.shape[0], -1)], axis=1)
 
 
-def mlp_fp8(layers, x, skip=None, round_input=True):
-    """The mixed fp8 network.  The paper leaves lower bit widths as future
-    headroom (Sec. 6.1) and fixes no scheme; this one keeps the first and the
-    last layer in bf16 (weights, inputs and skip rounded to bf16) and runs
-    the hidden layers in fp8: weights by ``quantize_fp8_weights``, inputs in
-    E4M3.  Each activation after bias and ReLU is clamped to 448 and rounded
-    to E4M3 where an fp8 layer reads it; where the last layer reads it, it is
-    rounded to bf16 (no clamp).  Sums accumulate in fp64."""
-    n = len(layers)
-    h = round_bf16(x) if round_input else np.asarray(x, dtype=np.float64)
-    for li, (W, b) in enumerate(layers):
-        if li == n - 1 and skip is not None:
-            h = np.concatenate([h, round_bf16(skip)], axis=1)
-        Wq = round_bf16(W) if li in (0, n - 1) else quantize_fp8_weights(W)
-        y = h @ Wq.T + b
-        if li < n - 1:
-            r = np.maximum(y, 0.0)
-            h = round_bf16(r) if li == n - 2 else round_e4m3(np.minimum(r, E4M3_MAX))
-        else:
-            h = y
-    return h
+# ---------------------------------------------------------------- rounding validity (checking aids)
+
+U_ACC = 2.0 ** -23
+
+
+def accumulation_bound(h, Wq, b):
+    """Bound on the error of the pre-activations Wq h + b when each is summed
+    in fp32 in any order: for n terms, |fl(sum) - sum| <= gamma_(n-1) sum |terms|
+    with gamma_k = k u / (1 - k u) (Higham, Accuracy and Stability of
+    Numerical Algorithms, 2nd ed., Sec. 3.1).  n = K + 2 (K products, the
+    bias, one spare rounding for fp32 products, which are not exact) and
+    u = 2^-23, which covers round-to-nearest and truncating adders alike.
+    A checking aid, not part of the method."""
+    Wq = np.asarray(Wq, dtype=np.float64)
+    n = Wq.shape[1] + 2
+    gamma = n * U_ACC / (1.0 - n * U_ACC)
+    return gamma * (np.abs(h) @ np.abs(Wq).T + np.abs(np.asarray(b, dtype=np.float64)))
+
+
+def valid_activations(y, beta, rounding):
+    """The outputs [lo, hi] a unit with exact pre-activation y may take when
+    its sum carries an error of at most beta: ``activation`` is monotone, so
+    every value it takes on [y - beta, y + beta] lies between its values at
+    the ends; lo == hi where no rounding midpoint (and no ReLU or clamp edge)
+    lies within beta of y.  A checking aid."""
+    return activation(y - beta, rounding), activation(y + beta, rounding)
 
 
 # ---------------------------------------------------------------- selection
@@ -336,8 +433,10 @@ def topn(logits, N):
 
 def softmax_fp32(logits):
     """Softmax over the classes in fp32: subtract the row maximum, exponentiate,
-    sum in class order, divide.  Strictly monotone, so the top-N of the
-    probabilities is the top-N of the logits."""
+    sum in class order, divide.  Monotone in exact arithmetic; in fp32 it can
+    map distinct logits to equal probabilities, so the selection of the
+    softmax workload ranks the logits (``topn``) and this only transforms the
+    scores it reports."""
     x = np.asarray(logits, dtype=F32)
     m = x.max(axis=1, keepdims=True)
     e = np.exp(x - m).astype(F32)
@@ -429,7 +528,7 @@ def composite(raw, t, delta):
 
 def render_rays(d_layers, s_layers, o, r, N, near, far, n_bins, centre, radius,
                 precision="fp64", select="topn", forced_bins=None, forced_samples=None,
-                depth_input="encoded"):
+                depth_input="encoded", jitter=None):
     """Per-ray inference for rays (o, r) (fp32, (n, 3)).  Returns dict with
     rgb (n,3), depth (n,), bins (n,N) int32, logits (n,B) fp64, the sample
     depths t and widths delta (n,N) and, for select='topn_softmax', probs
@@ -437,7 +536,8 @@ def render_rays(d_layers, s_layers, o, r, N, near, far, n_bins, centre, radius,
     forced_samples = (t, delta) overrides the placement (for comparisons).
     depth_input='positions' feeds the depth network the paper's unencoded
     input (``depth_positions_input``); in bf16 mode that input is not
-    rounded (only the weights and hidden activations are)."""
+    rounded (only the weights and hidden activations are).  ``jitter`` is
+    passed to both networks (``mlp``)."""
     d_max = F32(far)
     c = np.asarray(centre, dtype=F32)
     # 1-2: unification and the depth-network input (Eq. 2 / Sec. 5.2).
@@ -454,7 +554,7 @@ def render_rays(d_layers, s_layers, o, r, N, near, far, n_bins, centre, radius,
     else:
         raise ValueError(depth_input)
     # 3: depth oracle network -> class scores.
-    logits = mlp(d_layers, x0, precision, round_input=round_in)
+    logits = mlp(d_layers, x0, precision, round_input=round_in, jitter=jitter)
     out = {"logits": logits}
     # 4: selection of N classes.
     lg32 = logits.astype(F32)
@@ -483,7 +583,7 @@ def render_rays(d_layers, s_layers, o, r, N, near, far, n_bins, centre, radius,
     n = o.shape[0]
     feats = encode(w.reshape(n * N, 3), L_POS)
     skip = np.repeat(enc_r, N, axis=0)
-    raw = mlp(s_layers, feats, precision, skip=skip).reshape(n, N, 4)
+    raw = mlp(s_layers, feats, precision, skip=skip, jitter=jitter).reshape(n, N, 4)
     # 7: compositing.
     C, D, _ = composite(raw, t, delta)
     out["rgb"] = C
@@ -494,7 +594,7 @@ def render_rays(d_layers, s_layers, o, r, N, near, far, n_bins, centre, radius,
 def render(weights, poses, H, W, N, n_bins=128, near=0.1, far=10.0, fov_x_deg=60.0,
            centre=(0.0, 0.0, 0.0), radius=1.5, precision="fp64", select="topn",
            forced_bins=None, ray_subset=None, chunk=8192, forced_samples=None,
-           depth_input="encoded"):
+           depth_input="encoded", jitter=None):
     """Render P poses (P, 3, 4) of H x W rays.  Returns rgb (P*H*W, 3), depth,
     bins and logits for every ray (or for ``ray_subset``, global ray ids)."""
     d_layers, s_layers = split_weights(weights, n_bins, depth_input)
@@ -516,7 +616,7 @@ def render(weights, poses, H, W, N, n_bins=128, near=0.1, far=10.0, fov_x_deg=60
         part = render_rays(d_layers, s_layers, o[sl], r[sl], N, near, far, n_bins,
                            centre, radius, precision, select,
                            None if fb is None else fb[s:s + chunk],
-                           None if fs is None else (fs[0][sl], fs[1][sl]), depth_input)
+                           None if fs is None else (fs[0][sl], fs[1][sl]), depth_input, jitter)
         for k, val in part.items():
             res.setdefault(k, []).append(val)
     return {k: np.concatenate(v) for k, v in res.items()}

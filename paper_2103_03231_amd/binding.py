@@ -254,8 +254,26 @@ class Renderer:
             out["samples"] = t.empty((P, H, W, N, 2), dtype=t.float32, device=dev)
         return out
 
+    def _check_out(self, P, H, W, N, out):
+        """Reject output tensors the library would write out of bounds:
+        each present one must be a contiguous CUDA tensor of the right dtype
+        holding P x H x W x {3, 1, N, B, 2 N} values."""
+        t = self.torch
+        per_ray = {"rgb": 3, "depth": 1, "bins": N, "scores": self.cfg.n_bins, "samples": 2 * N}
+        if "rgb" not in out:
+            raise ValueError("out needs an 'rgb' tensor")
+        for k, v in out.items():
+            if k not in per_ray:
+                raise ValueError(f"unknown output {k!r}")
+            dtype = t.int32 if k == "bins" else t.float32
+            if not (isinstance(v, t.Tensor) and v.is_cuda and v.is_contiguous() and v.dtype == dtype):
+                raise ValueError(f"out[{k!r}] must be a contiguous CUDA {dtype} tensor")
+            if v.numel() != P * H * W * per_ray[k]:
+                raise ValueError(f"out[{k!r}] holds {v.numel()} values, the render writes {P * H * W * per_ray[k]}")
+
     def render_into(self, poses, H, W, N, out, debug=False):
         P = int(np.asarray(poses).reshape(-1, 12).shape[0])
+        self._check_out(P, H, W, N, out)
         ptr = lambda k: out[k].data_ptr() if k in out else None
         if debug:
             donerf_render_debug(self.h, poses, P, H, W, N, ptr("rgb"), ptr("depth"),

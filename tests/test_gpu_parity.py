@@ -1,10 +1,19 @@
 """Parity of the HIP path (through the C ABI) with the CPU oracle.
 
-Selection is compared bit for bit on identical scores.  End to end, rays
-whose selected classes differ from the oracle's (near-tied scores, "flips")
-are re-rendered by the oracle with the GPU's selection forced; RGB must then
-agree within 1e-4 (fp32 path, against the fp64 oracle) or 2e-2 (bf16 path,
-against the bf16-rounding oracle) on every ray.
+Every end-to-end check compares each step with the oracle per ray:
+
+* selection: the classes the render kernel selected equal, bit for bit, the
+  oracle's top-N of the scores the same launch dumped;
+* depth-network scores against the oracle's logits: within 1e-5 in fp32; in
+  bf16 and fp8 networks each ray passes the validity rule of
+  ``validity.check_rays`` (equal to the nominal evaluation within 1e-5, or a
+  valid evaluation reproducing it is exhibited, or within twice the spread of
+  valid evaluations);
+* RGB and depth with the GPU's selection (or inverse-CDF samples) forced on
+  the oracle ("teacher forcing"): within 1e-4 (RGB) and 1e-3 (depth) in fp32,
+  the contract's tolerances; in bf16 within 2e-2 and 0.2, and per ray the
+  validity rule at 1e-4; in the mixed fp8 network per ray the validity rule;
+* rays whose oracle selection differs (near-tied scores) are counted.
 """
 import sys
 
@@ -12,18 +21,22 @@ import numpy as np
 import pytest
 import torch
 
+import validity
 from oracle import donerf_oracle as O
 from paper_2103_03231_amd import binding as b
 from paper_2103_03231_amd import inputs
 
 pytestmark = pytest.mark.gpu
 
-# RGB bars: the contract's fp32 and bf16 tolerances; the fp8 network's bar
-# is a distribution (FP8_BAR, see check_fp8).
-TOL = {"fp32": 1e-4, "bf16": 2e-2, "fp8": 2e-2}
+# the contract's RGB tolerances (fp32 path against the fp64 oracle, bf16
+# path against the bf16-rounding oracle); depth = sum w t with t <= d_max = 10
+# gets ten times that
+TOL = {"fp32": 1e-4, "bf16": 2e-2}
 PREC = {"fp32": b.FP32, "bf16": b.BF16, "fp8": b.FP8}
-# share of rays whose selection may differ from the oracle's (near ties)
+# share of rays whose oracle selection may differ from the GPU's (near ties)
 FLIPS = {"fp32": 0.0, "bf16": 0.03, "fp8": 0.05}
+# fp32 scores: a few fp32 roundings of sums of magnitude ~5 (measured 3e-6)
+SCORE_TOL_FP32 = 1e-5
 
 
 def log(*a):
@@ -47,30 +60,68 @@ def gpu_render(r, poses, H, W, N):
     return {k: v.cpu().numpy() for k, v in out.items()}
 
 
-def check_against_oracle(g, w, poses, H, W, N, precision, n_bins=128, fov=60.0, subset=None,
-                         max_flip_frac=0.0, label="", depth_input="encoded"):
-    gb = g["bins"].reshape(-1, N)
-    rgb = g["rgb"].reshape(-1, 3)
-    depth = g["depth"].reshape(-1)
-    scores = g["scores"].reshape(-1, n_bins) if "scores" in g else None
-    if subset is not None:
-        gb, rgb, depth = gb[subset], rgb[subset], depth[subset]
-        scores = None if scores is None else scores[subset]
-    ora = O.render(w, poses, H, W, N, n_bins=n_bins, fov_x_deg=fov, precision=precision,
-                   forced_bins=gb, ray_subset=subset, depth_input=depth_input)
-    natural = O.topn(ora["logits"].astype(np.float32), N)
-    flips = np.any(natural != gb, axis=1)
+def _rgbd(rgb, depth):
+    """Per-ray vector of RGB and depth / d_max (depth on the RGB scale)."""
+    return np.concatenate([np.asarray(rgb, np.float64).reshape(-1, 3),
+                           np.asarray(depth, np.float64).reshape(-1, 1) / 10.0], axis=1)
+
+
+def check_scores(scores, ora, precision, rerun, label):
+    """Depth-network scores of each ray against the oracle's logits."""
+    serr = np.abs(scores - ora["logits"]).max(axis=1)
+    if precision == "fp32":
+        log(f"[{label}] scores maxabs {serr.max():.3e}")
+        assert serr.max() <= SCORE_TOL_FP32, serr.max()
+        return
+    st = validity.check_rays(scores, ora["logits"], rerun, tol=SCORE_TOL_FP32, seed=1)
+    log(f"[{label}] scores {st}")
+
+
+def check_colour(rgb, depth, ora, precision, rerun, label):
+    """Teacher-forced RGB and depth of each ray against the oracle."""
     err = np.abs(rgb - ora["rgb"]).max()
     derr = np.abs(depth - ora["depth"]).max()
-    serr = np.nan if scores is None else np.abs(scores - ora["logits"]).max()
-    log(f"[{label}] rays={len(gb)} flips={flips.sum()} rgb_maxabs={err:.3e} depth_maxabs={derr:.3e} "
-        f"score_maxabs={serr:.3e}")
     assert np.all(np.isfinite(rgb)) and np.all((rgb >= 0) & (rgb <= 1))
+    if precision in TOL:
+        log(f"[{label}] rgb maxabs {err:.3e} depth maxabs {derr:.3e}")
+        assert err <= TOL[precision], err
+        assert derr <= 10.0 * TOL[precision], derr
+    if precision != "fp32":
+        st = validity.check_rays(_rgbd(rgb, depth), _rgbd(ora["rgb"], ora["depth"]), rerun, tol=1e-4, seed=2)
+        log(f"[{label}] rgb+depth {st}")
+
+
+def check_against_oracle(g, w, poses, H, W, N, precision, n_bins=128, fov=60.0, subset=None,
+                         max_flip_frac=0.0, label="", depth_input="encoded", raw_scores=True):
+    """g: the GPU's per-ray outputs (bins, scores, rgb, depth) of all rays, or
+    of ``subset`` (global ray ids) only when they are already that long.
+    raw_scores: false when the dumped scores are softmax probabilities."""
+    gb = g["bins"].reshape(-1, N)
+    rgb = g["rgb"].reshape(-1, 3).astype(np.float64)
+    depth = g["depth"].reshape(-1).astype(np.float64)
+    scores = g["scores"].reshape(-1, n_bins).astype(np.float64)
+    ids = np.arange(len(gb)) if subset is None else np.asarray(subset)
+    if len(gb) != len(ids):
+        gb, rgb, depth, scores = gb[ids], rgb[ids], depth[ids], scores[ids]
+    kw = dict(n_bins=n_bins, fov_x_deg=fov, precision=precision, depth_input=depth_input)
+    ora = O.render(w, poses, H, W, N, forced_bins=gb, ray_subset=ids, **kw)
+
+    def rerun(key):
+        def f(idx, rng, rho):
+            r = O.render(w, poses, H, W, N, forced_bins=gb[idx], ray_subset=ids[idx], jitter=(rng, rho), **kw)
+            return r["logits"] if key == "logits" else _rgbd(r["rgb"], r["depth"])
+        return f
+
+    if raw_scores:
+        # the render kernel's own selection, on the scores the same launch dumped
+        assert np.array_equal(O.topn(scores.astype(np.float32), N), gb)
+        check_scores(scores, ora, precision, rerun("logits"), label)
+    natural = O.topn(ora["logits"].astype(np.float32), N)
+    flips = np.any(natural != gb, axis=1)
+    log(f"[{label}] rays={len(gb)} oracle selection differs on {flips.sum()}")
     assert flips.mean() <= max_flip_frac, flips.mean()
-    assert err <= TOL[precision], err
-    # depth = sum w t with t <= d_max: the same relative tolerance
-    assert derr <= TOL[precision] * 10.0, derr
-    return err, flips
+    check_colour(rgb, depth, ora, precision, rerun("rgb"), label)
+    return flips
 
 
 # ------------------------------------------------------------------ depth classes
@@ -229,7 +280,8 @@ def test_render_on_a_side_stream():
 
 def test_render_rejects_bad_sizes():
     """Empty frames and frames beyond the stated limits (P H W < 2^31,
-    H W <= 2^24) fail before any launch."""
+    H W <= 2^24) fail before any launch; the Python owner rejects output
+    tensors that do not match the frame before calling the library."""
     r, _ = renderer("bf16", n_max=4)
     out = r.alloc(1, 2, 2, 4)
     for P, H, W in ((0, 8, 8), (1, 0, 8), (1, 8, -1), (200, 4096, 4096), (1, 8192, 8192)):
@@ -237,6 +289,18 @@ def test_render_rejects_bad_sizes():
         with pytest.raises(b.DonerfError) as e:
             b.donerf_render(r.h, poses, P, H, W, 4, out["rgb"].data_ptr())
         assert e.value.status == b.E_INVALID_ARG, (P, H, W)
+    poses = inputs.make_poses([0])
+    good = r.alloc(1, 4, 4, 4, depth=True, debug=True)
+    bad = [("rgb", torch.empty((1, 4, 4, 2), dtype=torch.float32, device="cuda")),
+           ("depth", torch.empty((1, 4, 5), dtype=torch.float32, device="cuda")),
+           ("bins", torch.empty((1, 4, 4, 4), dtype=torch.float32, device="cuda")),
+           ("scores", torch.empty((1, 4, 4, 128), dtype=torch.float32)),
+           ("samples", torch.empty((1, 4, 4, 8, 2), dtype=torch.float32, device="cuda")[:, :, :, ::2])]
+    for k, v in bad:
+        with pytest.raises(ValueError):
+            r.render_into(poses, 4, 4, 4, {**good, k: v}, debug=True)
+    r.render_into(poses, 4, 4, 4, good, debug=True)
+    torch.cuda.synchronize()
     r.close()
 
 
@@ -276,40 +340,54 @@ def test_transparent_and_opaque_scenes(precision):
 
 # ------------------------------------------------------------------ full-size workloads, sampled
 
-def _sampled(workload, n_sample, seed=0):
-    wl = inputs.WORKLOADS[workload]
-    r, w = renderer(wl.precision, n_bins=wl.n_bins, n_max=wl.N, fov=wl.fov_deg,
-                    select=b.SELECT_TOPN_SOFTMAX if wl.select == "topn_softmax" else b.SELECT_TOPN,
-                    depth_input=wl.depth_input)
-    poses = wl.poses()
-    if wl.name.startswith("stereo"):
-        poses = poses[:2]            # one stereo pair of the 60-pose sequence
+def _render_subset(r, wl, poses, subset, debug_scores=True):
+    """Render the whole workload frame on the GPU (the bench's launch shape)
+    and return the per-ray outputs of ``subset``."""
     P = len(poses)
-    out = r.alloc(P, wl.H, wl.W, wl.N, depth=True)
-    out["bins"] = torch.empty((P, wl.H, wl.W, wl.N), dtype=torch.int32, device="cuda")
-    log(f"[{workload}] rendering {P}x{wl.H}x{wl.W} N={wl.N} B={wl.n_bins}")
+    out = r.alloc(P, wl.H, wl.W, wl.N, depth=True, debug=True)
+    if not debug_scores:
+        del out["scores"]
     r.render_into(poses, wl.H, wl.W, wl.N, out, debug=True)
     torch.cuda.synchronize()
     rgb = out["rgb"].reshape(-1, 3)
     assert bool(torch.isfinite(rgb).all()) and float(rgb.min()) >= 0 and float(rgb.max()) <= 1
-    rng = np.random.default_rng(seed)
-    total = P * wl.H * wl.W
-    subset = np.unique(np.concatenate([rng.integers(0, total, n_sample), [0, total - 1]]))
     sub = torch.from_numpy(subset).cuda()
-    g = {"rgb": out["rgb"].reshape(-1, 3)[sub].cpu().numpy(),
-         "depth": out["depth"].reshape(-1)[sub].cpu().numpy(),
-         "bins": out["bins"].reshape(-1, wl.N)[sub].cpu().numpy()}
-    gb = g["bins"]
-    ora = O.render(w, poses, wl.H, wl.W, wl.N, n_bins=wl.n_bins, fov_x_deg=wl.fov_deg,
-                   precision=wl.precision, forced_bins=gb, ray_subset=subset, depth_input=wl.depth_input)
-    flips = np.any(O.topn(ora["logits"].astype(np.float32), wl.N) != gb, axis=1)
-    err = np.abs(g["rgb"] - ora["rgb"]).max()
-    derr = np.abs(g["depth"] - ora["depth"]).max()
-    log(f"[{workload}] sampled={len(subset)} flips={flips.sum()} rgb_maxabs={err:.3e} depth_maxabs={derr:.3e}")
-    assert err <= TOL[wl.precision]
-    assert derr <= 10 * TOL[wl.precision]
-    assert flips.mean() <= 0.03
+    g = {k: v.reshape(P * wl.H * wl.W, -1)[sub].cpu().numpy() for k, v in out.items()}
+    del out
+    torch.cuda.empty_cache()
+    return g
+
+
+def _sampled(workload, n_sample, seed=0):
+    wl = inputs.WORKLOADS[workload]
+    softmax = wl.select == "topn_softmax"
+    r, w = renderer(wl.precision, n_bins=wl.n_bins, n_max=wl.N, fov=wl.fov_deg,
+                    select=b.SELECT_TOPN_SOFTMAX if softmax else b.SELECT_TOPN, depth_input=wl.depth_input)
+    poses = wl.poses()
+    if wl.name.startswith("stereo"):
+        poses = poses[:2]            # one stereo pair of the 60-pose sequence
+    P = len(poses)
+    total = P * wl.H * wl.W
+    rng = np.random.default_rng(seed)
+    subset = np.unique(np.concatenate([rng.integers(0, total, n_sample), [0, total - 1]]))
+    log(f"[{workload}] rendering {P}x{wl.H}x{wl.W} N={wl.N} B={wl.n_bins}, checking {len(subset)} rays")
+    g = _render_subset(r, wl, poses, subset)
     r.close()
+    if softmax:
+        # the softmax only transforms the dumped scores: a top-N handle of the
+        # same weights selects and renders the same, and dumps the raw scores
+        probs = g["scores"]
+        rt, _ = renderer(wl.precision, n_bins=wl.n_bins, n_max=wl.N, fov=wl.fov_deg, select=b.SELECT_TOPN,
+                         depth_input=wl.depth_input)
+        gt = _render_subset(rt, wl, poses, subset)
+        rt.close()
+        for k in ("bins", "rgb", "depth"):
+            assert np.array_equal(g[k], gt[k]), k
+        np.testing.assert_allclose(probs, O.softmax_fp32(gt["scores"]), rtol=1e-5, atol=1e-8)
+        g = gt
+    check_against_oracle(g, w, poses, wl.H, wl.W, wl.N, wl.precision, n_bins=wl.n_bins, fov=wl.fov_deg,
+                         subset=subset, max_flip_frac=FLIPS[wl.precision], label=workload,
+                         depth_input=wl.depth_input)
 
 
 def test_frame400_n4_bf16_sampled():
@@ -364,30 +442,63 @@ def _log_coord(t, near=0.1, far=10.0):
 CDF_COORD_TOL = 3e-4
 
 
-def check_cdf(g, w, poses, H, W, N, precision, n_bins=128, subset=None, label=""):
-    scores = g["scores"].reshape(-1, n_bins)
-    samp = g["samples"].reshape(-1, N, 2)
-    rgb = g["rgb"].reshape(-1, 3)
-    depth = g["depth"].reshape(-1)
-    if subset is not None:
-        scores, samp, rgb, depth = scores[subset], samp[subset], rgb[subset], depth[subset]
-    t_ref, d_ref, _ = O.cdf_samples(scores, N, 0.1, 10.0)
+def check_cdf(g, w, poses, H, W, N, precision, n_bins=128, subset=None, label="", depth_input="encoded"):
+    """Inverse-CDF placement, step by step against the oracle:
+    * scores against the oracle's logits, per ray (``check_scores``);
+    * the placement on the GPU's own scores (identical inputs) against the
+      oracle's inverse CDF, in the Eq. 3 coordinate, and in fp32 also against
+      the oracle's placement on its own logits, with the same classes except
+      where the oracle's sample lies within the tolerance of a class bound;
+    * RGB and depth with the GPU's samples forced on the oracle
+      (``check_colour``)."""
+    scores = g["scores"].reshape(-1, n_bins).astype(np.float64)
+    samp = g["samples"].reshape(-1, N, 2).astype(np.float64)
+    cls = g["bins"].reshape(-1, N)
+    rgb = g["rgb"].reshape(-1, 3).astype(np.float64)
+    depth = g["depth"].reshape(-1).astype(np.float64)
+    ids = np.arange(len(scores)) if subset is None else np.asarray(subset)
+    if len(scores) != len(ids):
+        scores, samp, cls, rgb, depth = scores[ids], samp[ids], cls[ids], rgb[ids], depth[ids]
+    kw = dict(n_bins=n_bins, precision=precision, select="cdf", depth_input=depth_input)
+    # the depth network and the oracle's own placement
+    nat = O.render(w, poses, H, W, N, ray_subset=ids, **kw)
+
+    def rerun_logits(idx, rng, rho):
+        return O.render(w, poses, H, W, N, ray_subset=ids[idx], jitter=(rng, rho),
+                        forced_samples=(samp[idx, :, 0], samp[idx, :, 1]), **kw)["logits"]
+
+    check_scores(scores, nat, precision, rerun_logits, label)
+    # the placement on identical scores
+    t_ref, d_ref, c_ref = O.cdf_samples(scores.astype(np.float32), N, 0.1, 10.0)
     cerr = np.abs(_log_coord(samp[..., 0]) - _log_coord(t_ref)).max()
-    # widths: differences of two such depths
-    derr = np.abs(samp[..., 1] - d_ref).max()
-    dtol = 2 * CDF_COORD_TOL * np.log(10.0 - 0.1 + 1.0) * 10.9
-    ora = O.render(w, poses, H, W, N, n_bins=n_bins, precision=precision, select="cdf",
-                   forced_samples=(samp[..., 0], samp[..., 1]), ray_subset=subset)
-    err = np.abs(rgb - ora["rgb"]).max()
-    zerr = np.abs(depth - ora["depth"]).max()
-    log(f"[{label}] rays={len(scores)} coord_maxabs={cerr:.3e} width_maxabs={derr:.3e} "
-        f"rgb_maxabs={err:.3e} depth_maxabs={zerr:.3e}")
+    werr = np.abs(samp[..., 1] - d_ref).max()
+    wtol = 2 * CDF_COORD_TOL * np.log(10.0 - 0.1 + 1.0) * 10.9
+    log(f"[{label}] placement on the GPU's scores: coord maxabs {cerr:.3e} width maxabs {werr:.3e}")
     assert np.all(np.diff(samp[..., 0], axis=1) >= 0)
     np.testing.assert_allclose(samp[..., 1].sum(1), float(np.float32(10.0)) - float(np.float32(0.1)), rtol=1e-4)
     assert cerr <= CDF_COORD_TOL, cerr
-    assert derr <= dtol, derr
-    assert err <= TOL[precision], err
-    assert zerr <= 10 * TOL[precision], zerr
+    assert werr <= wtol, werr
+    if precision == "fp32":
+        s_nat = _log_coord(nat["t"])
+        nerr = np.abs(_log_coord(samp[..., 0]) - s_nat).max()
+        # classes must agree unless the oracle's sample sits within the
+        # coordinate tolerance of a class bound (k / B)
+        frac = s_nat * n_bins - np.floor(s_nat * n_bins)
+        near_bound = np.minimum(frac, 1.0 - frac) / n_bins <= CDF_COORD_TOL
+        bad = (cls != nat["bins"]) & ~near_bound
+        log(f"[{label}] placement on the oracle's logits: coord maxabs {nerr:.3e}, "
+            f"classes differ {int((cls != nat['bins']).sum())} (all within the tolerance of a bound)")
+        assert nerr <= CDF_COORD_TOL, nerr
+        assert not bad.any(), np.nonzero(bad)
+    # colour with the GPU's samples forced
+    ora = O.render(w, poses, H, W, N, ray_subset=ids, forced_samples=(samp[..., 0], samp[..., 1]), **kw)
+
+    def rerun_rgb(idx, rng, rho):
+        r = O.render(w, poses, H, W, N, ray_subset=ids[idx], jitter=(rng, rho),
+                     forced_samples=(samp[idx, :, 0], samp[idx, :, 1]), **kw)
+        return _rgbd(r["rgb"], r["depth"])
+
+    check_colour(rgb, depth, ora, precision, rerun_rgb, label)
 
 
 @pytest.mark.parametrize("precision", ["fp32", "bf16"])
@@ -416,14 +527,10 @@ def test_frame400_n4_cdf_bf16_sampled():
     wl = inputs.WORKLOADS["frame400_n4_cdf_bf16"]
     r, w = renderer(wl.precision, n_bins=wl.n_bins, n_max=wl.N, select=b.SELECT_CDF)
     poses = wl.poses()
-    P = len(poses)
-    out = r.alloc(P, wl.H, wl.W, wl.N, depth=True, debug=True)
-    r.render_into(poses, wl.H, wl.W, wl.N, out, debug=True)
-    torch.cuda.synchronize()
-    g = {k: v.cpu().numpy() for k, v in out.items()}
-    subset = np.unique(np.random.default_rng(3).integers(0, P * wl.H * wl.W, 1500))
-    check_cdf(g, w, poses, wl.H, wl.W, wl.N, wl.precision, subset=subset, label=wl.name)
+    subset = np.unique(np.random.default_rng(3).integers(0, len(poses) * wl.H * wl.W, 1500))
+    g = _render_subset(r, wl, poses, subset)
     r.close()
+    check_cdf(g, w, poses, wl.H, wl.W, wl.N, wl.precision, subset=subset, label=wl.name)
 
 
 # ------------------------------------------------------------------ depth-network input features
@@ -550,15 +657,7 @@ def test_positions_variants(precision, N, B, H, W, P, select):
     g = gpu_render(r, poses, H, W, N)
     label = f"positions {select} {precision} N={N} B={B} {P}x{H}x{W}"
     if select == "cdf":
-        samp = g["samples"].reshape(-1, N, 2)
-        t_ref, _, _ = O.cdf_samples(g["scores"].reshape(-1, B), N, 0.1, 10.0)
-        cerr = np.abs(_log_coord(samp[..., 0]) - _log_coord(t_ref)).max()
-        ora = O.render(w, poses, H, W, N, n_bins=B, precision=precision, select="cdf",
-                       forced_samples=(samp[..., 0], samp[..., 1]), depth_input="positions")
-        err = np.abs(g["rgb"].reshape(-1, 3) - ora["rgb"]).max()
-        serr = np.abs(g["scores"].reshape(-1, B) - ora["logits"]).max()
-        log(f"[{label}] coord_maxabs={cerr:.3e} rgb_maxabs={err:.3e} score_maxabs={serr:.3e}")
-        assert cerr <= CDF_COORD_TOL and err <= TOL[precision]
+        check_cdf(g, w, poses, H, W, N, precision, n_bins=B, label=label, depth_input="positions")
     else:
         check_against_oracle(g, w, poses, H, W, N, precision, n_bins=B, label=label,
                              max_flip_frac=FLIPS[precision], depth_input="positions")
@@ -567,29 +666,6 @@ def test_positions_variants(precision, N, B, H, W, P, select):
 
 # ------------------------------------------------------------------ the mixed fp8 network
 
-# The fp8 network's rounding is discontinuous at the scale that matters: an
-# accumulation-order difference (fp32 MFMA vs the oracle's fp64) that
-# straddles an E4M3 rounding boundary moves that activation by a whole E4M3
-# step (1/16 to 1/8 of it), which shifts every pre-activation of the next
-# layer by about W x that step and flips further roundings there.  Most rays
-# agree to fp32 noise; a few per cent cascade into another, equally valid,
-# fp8 evaluation.  The bar is therefore a distribution: the median ray within
-# 1e-3 (with 16 samples per ray about half the rays hold one diverged
-# sample; with 4, the median ray agrees to 1e-5), the 99th percentile within
-# the bf16 bar, every ray within 5e-2, or 0.25 with inverse-CDF slices, whose
-# widths (up to ~5 against class widths <= 0.2) multiply the density
-# difference of a diverged sample.
-FP8_BAR = {"p50": 1e-3, "p99": 2e-2, "max_topn": 5e-2, "max_cdf": 0.25}
-
-
-def check_fp8(err, label, cdf=False):
-    p50, p99 = np.percentile(err, 50), np.percentile(err, 99)
-    log(f"[{label}] rgb p50={p50:.2e} p99={p99:.2e} max={err.max():.2e}")
-    assert p50 <= FP8_BAR["p50"], p50
-    assert p99 <= FP8_BAR["p99"], p99
-    assert err.max() <= FP8_BAR["max_cdf" if cdf else "max_topn"], err.max()
-
-
 @pytest.mark.parametrize("N,B,H,W,P,select,din", [
     (4, 128, 32, 32, 1, "topn", "encoded"),
     (1, 64, 17, 23, 1, "topn", "encoded"),
@@ -597,49 +673,29 @@ def check_fp8(err, label, cdf=False):
     (16, 192, 12, 20, 2, "topn", "encoded"),
     (4, 128, 24, 40, 1, "topn", "positions"),
     (4, 128, 24, 40, 1, "cdf", "encoded"),
+    (16, 128, 12, 20, 1, "cdf", "encoded"),
 ])
 def test_fp8_variants(N, B, H, W, P, select, din):
     """fp8 path against the oracle's fp8 network (same rounding points: E4M3
     weights with the same per-layer scales, E4M3 activations clamped to 448,
-    bf16 first layers and heads), teacher-forced on the GPU's selection or
-    samples, to FP8_BAR; up to 5 % of rays may select differently."""
+    bf16 first layers and heads): scores and teacher-forced colour per ray by
+    the validity rule, selection and placement on identical scores exactly
+    as in bf16."""
     sel = b.SELECT_CDF if select == "cdf" else b.SELECT_TOPN
     r, w = renderer("fp8", n_bins=B, n_max=max(N, 4), select=sel, seed=5, depth_input=din)
     poses = inputs.make_poses(list(range(30, 30 + P)))
     g = gpu_render(r, poses, H, W, N)
+    r.close()
     label = f"fp8 {select} {din} N={N} B={B} {P}x{H}x{W}"
     if select == "cdf":
-        samp = g["samples"].reshape(-1, N, 2)
-        t_ref, _, _ = O.cdf_samples(g["scores"].reshape(-1, B), N, 0.1, 10.0)
-        cerr = np.abs(_log_coord(samp[..., 0]) - _log_coord(t_ref)).max()
-        assert cerr <= CDF_COORD_TOL, cerr
-        ora = O.render(w, poses, H, W, N, n_bins=B, precision="fp8", select="cdf",
-                       forced_samples=(samp[..., 0], samp[..., 1]), depth_input=din)
+        check_cdf(g, w, poses, H, W, N, "fp8", n_bins=B, label=label, depth_input=din)
     else:
-        gb = g["bins"].reshape(-1, N)
-        ora = O.render(w, poses, H, W, N, n_bins=B, precision="fp8", forced_bins=gb, depth_input=din)
-        flips = np.any(O.topn(ora["logits"].astype(np.float32), N) != gb, axis=1)
-        log(f"[{label}] flips={flips.sum()} of {len(gb)}")
-        assert flips.mean() <= FLIPS["fp8"]
-    check_fp8(np.abs(g["rgb"].reshape(-1, 3) - ora["rgb"]).max(1), label, cdf=select == "cdf")
-    r.close()
+        check_against_oracle(g, w, poses, H, W, N, "fp8", n_bins=B, label=label, max_flip_frac=FLIPS["fp8"],
+                             depth_input=din)
 
 
-def test_fp8_frame400_sampled():
-    r, w = renderer("fp8")
-    poses = inputs.make_poses(range(5))
-    out = r.alloc(5, 400, 400, 4, depth=True)
-    out["bins"] = torch.empty((5, 400, 400, 4), dtype=torch.int32, device="cuda")
-    r.render_into(poses, 400, 400, 4, out, debug=True)
-    torch.cuda.synchronize()
-    g = {k: v.cpu().numpy() for k, v in out.items()}
-    subset = np.unique(np.random.default_rng(4).integers(0, 5 * 400 * 400, 2000))
-    gb = g["bins"].reshape(-1, 4)[subset]
-    ora = O.render(w, poses, 400, 400, 4, precision="fp8", forced_bins=gb, ray_subset=subset)
-    flips = np.any(O.topn(ora["logits"].astype(np.float32), 4) != gb, axis=1)
-    assert flips.mean() <= FLIPS["fp8"]
-    check_fp8(np.abs(g["rgb"].reshape(-1, 3)[subset] - ora["rgb"]).max(1), "fp8 5x400x400")
-    r.close()
+def test_frame400_n4_fp8_sampled():
+    _sampled("frame400_n4_fp8", 2000)
 
 
 def test_fp8_tolerance_study():
