@@ -143,11 +143,11 @@ __device__ __forceinline__ void wait_vmcnt() {
 // The workgroup consumes one logical sequence of chunks: every depth-network
 // chunk, then the shading-network chunks once per sample.  Chunks travel
 // from L2 straight into LDS (global_load_lds, 16 bytes per lane) one chunk
-// ahead of use, alternating between two LDS arrays.  Every layer holds an
-// even number of chunks (padded with zeros), so chunk j of a layer always
-// sits in slot j & 1 and every read and copy names its array at compile
-// time: reads of one slot then carry a different alias scope from the copy
-// in flight into the other, and need no wait for it.  Each wave copies
+// ahead of use, alternating between two LDS arrays.  The slot of every chunk
+// is known at compile time (each layer is told the slot parity of its first
+// chunk; layout.h layer_chunks), so every read and copy names its array
+// statically: reads of one slot then carry a different alias scope from the
+// copy in flight into the other, and need no wait for it.  Each wave copies
 // kChunkFrags / NW fragments of every chunk; advancing to chunk c waits for
 // the wave's own copies of c and then barriers, which both publishes c and
 // retires every reader of chunk c - 1, whose slot the copy of c + 1 reuses.
@@ -200,6 +200,7 @@ struct WeightStream {
         issue<1 - PAR>();
     }
     __device__ __forceinline__ void finish() { wait_vmcnt<0>(); }
+
     template <int PAR>
     __device__ __forceinline__ u32x4 frag(int i) const {
         return (PAR ? ring1 : ring0)[i * 64 + lane];
@@ -331,7 +332,7 @@ __device__ __forceinline__ void emit_fp8(const f32x16& a0, const f32x16& a1, u32
 // output activations (the next layer's), MP that of the layer's own steps and
 // input; sa is the E8M0 scale of fp8 weights.  getB(k, c) returns the u32x4
 // k of the input (an fp8 step reads two).
-template <int OUT, int CB, int KS, int MP, class WS, class GetB, int NOUT>
+template <int OUT, int CB, int KS, int MP, int PAR0 = 0, bool PADDED = true, class WS, class GetB, int NOUT>
 __device__ __forceinline__ void hidden_layer(WS& st, int g, BiasAt bias, GetB&& getB,
                                              u32x4 (&out)[NOUT][CB], int sa = 127) {
     using M = Prec<MP>;
@@ -344,63 +345,68 @@ __device__ __forceinline__ void hidden_layer(WS& st, int g, BiasAt bias, GetB&& 
     static_assert(OUT != kFP8 || RBP == 2, "an fp8 K step takes two row blocks");
     f32x16 acc[2][RBP][CB];
     u32x4 a[D + 1][U];
+    auto load_bias = [&](auto PP) {
+        constexpr int q = CV(PP);
+        sfor<RBP>([&](auto R) {
+            const f32x16 b = bias_frag(bias + 32 * (RBP * q + CV(R)), g);
+            sfor<CB>([&](auto C) { acc[q & 1][CV(R)][CV(C)] = b; });
+        });
+    };
+    auto epilogue = [&](auto PP) {
+        constexpr int p = CV(PP);
+        if constexpr (OUT == kFP8) {
+            sfor<CB>([&](auto C) { emit_fp8(acc[p & 1][0][CV(C)], acc[p & 1][1][CV(C)], out, p, CV(C)); });
+            // Pin the pass's outputs here: layers outside a loop could
+            // otherwise have their pure MFMA chains sunk past the later chunk
+            // barriers to the blocks that use them, holding every fragment of
+            // those chunks in registers.
+            sfor<CB>([&](auto C) {
+                const u32x4 o0 = out[2 * p][CV(C)], o1 = out[2 * p + 1][CV(C)];
+                asm volatile("" ::"v"(o0), "v"(o1));
+            });
+        } else if constexpr (MP == kFP8) {
+            sfor<RBP>([&](auto R) {
+                sfor<CB>([&](auto C) {
+                    emit_relu<OUT>(acc[p & 1][CV(R)][CV(C)], out, (p * RBP + CV(R)) * Prec<OUT>::KSPB, CV(C));
+                    sfor<Prec<OUT>::KSPB>([&](auto H) {
+                        const u32x4 o = out[(p * RBP + CV(R)) * Prec<OUT>::KSPB + CV(H)][CV(C)];
+                        asm volatile("" ::"v"(o));
+                    });
+                });
+            });
+        } else {
+            sfor<RBP>([&](auto R) {
+                sfor<CB>([&](auto C) {
+                    emit_relu<OUT>(acc[p & 1][CV(R)][CV(C)], out, (p * RBP + CV(R)) * Prec<OUT>::KSPB, CV(C));
+                });
+            });
+        }
+    };
     sfor<NF + D>([&](auto S) {
         constexpr int s = CV(S);
         if constexpr (s < NF) {
-            if constexpr (s % SPC == 0) st.template next<(s / SPC) & 1>();
+            if constexpr (s % SPC == 0) st.template next<(s / SPC + PAR0) & 1>();
 #pragma unroll
-            for (int u = 0; u < U; ++u) a[s % (D + 1)][u] = st.template frag<(s / SPC) & 1>((s % SPC) * U + u);
+            for (int u = 0; u < U; ++u)
+                a[s % (D + 1)][u] = st.template frag<(s / SPC + PAR0) & 1>((s % SPC) * U + u);
         }
         if constexpr (s >= D) {
             constexpr int f = s - D;
             constexpr int p = f / PF, w = f % PF, k = w / RBP, r = w % RBP;
-            if constexpr (w == 0) {
-                sfor<RBP>([&](auto R) {
-                    const f32x16 b = bias_frag(bias + 32 * (RBP * p + CV(R)), g);
-                    sfor<CB>([&](auto C) { acc[p & 1][CV(R)][CV(C)] = b; });
-                });
-            }
+            if constexpr (w == 0) load_bias(std::integral_constant<int, p>{});
             sfor<CB>([&](auto C) {
                 u32x4 bk[U];
                 sfor<U>([&](auto V) { bk[CV(V)] = getB(std::integral_constant<int, k * U + CV(V)>{}, C); });
                 acc[p & 1][r][CV(C)] = M::mma(a[f % (D + 1)], bk, acc[p & 1][r][CV(C)], sa);
             });
-            if constexpr (w == PF - 1) {
-                if constexpr (OUT == kFP8) {
-                    sfor<CB>([&](auto C) { emit_fp8(acc[p & 1][0][CV(C)], acc[p & 1][1][CV(C)], out, p, CV(C)); });
-                    // Pin the pass's outputs here: layers outside a loop
-                    // could otherwise have their pure MFMA chains sunk past
-                    // the later chunk barriers to the blocks that use them,
-                    // holding every fragment of those chunks in registers.
-                    sfor<CB>([&](auto C) {
-                        const u32x4 o0 = out[2 * p][CV(C)], o1 = out[2 * p + 1][CV(C)];
-                        asm volatile("" ::"v"(o0), "v"(o1));
-                    });
-                } else if constexpr (MP == kFP8) {
-                    sfor<RBP>([&](auto R) {
-                        sfor<CB>([&](auto C) {
-                            emit_relu<OUT>(acc[p & 1][CV(R)][CV(C)], out, (p * RBP + CV(R)) * Prec<OUT>::KSPB,
-                                           CV(C));
-                            sfor<Prec<OUT>::KSPB>([&](auto H) {
-                                const u32x4 o = out[(p * RBP + CV(R)) * Prec<OUT>::KSPB + CV(H)][CV(C)];
-                                asm volatile("" ::"v"(o));
-                            });
-                        });
-                    });
-                } else {
-                    sfor<RBP>([&](auto R) {
-                        sfor<CB>([&](auto C) {
-                            emit_relu<OUT>(acc[p & 1][CV(R)][CV(C)], out, (p * RBP + CV(R)) * Prec<OUT>::KSPB,
-                                           CV(C));
-                        });
-                    });
-                }
-            }
+            if constexpr (w == PF - 1) epilogue(std::integral_constant<int, p>{});
         }
         __builtin_amdgcn_sched_barrier(0x6);
     });
-    // a layer of an odd number of chunks is padded to an even one
-    if constexpr (((NF * U + kChunkFrags - 1) / kChunkFrags) & 1) st.template next<1>();
+    // a layer of an odd number of chunks is padded to an even one (unless
+    // the stream omits that padding)
+    constexpr int CH = (NF * U + kChunkFrags - 1) / kChunkFrags;
+    if constexpr (PADDED && (CH & 1)) st.template next<(CH + PAR0) & 1>();
 }
 
 // ------------------------------------------------------------------ selection
@@ -833,26 +839,30 @@ render_kernel(const RenderArgs a) {
     auto g1 = [&](auto K, auto C) { return h1[CV(K)][CV(C)]; };
     // six 256 -> 256 ReLU layers whose biases start at bias_l0 and whose fp8
     // weight scales start at ws; the last one feeds a head in FP
-    auto hidden6 = [&](BiasAt bias_l0, const int32_t* ws) {
+    // (PAR: slot parity of the first chunk; every hidden layer streams an
+    // even number of chunks, so it holds for all six)
+    auto hidden6 = [&](auto PAR, BiasAt bias_l0, const int32_t* ws) {
+        constexpr int Q = CV(PAR);
         if constexpr (PR == kFP8) {
             for (int l = 0; l < 2; ++l) {
-                hidden_layer<kFP8, CB, KS_HID, kFP8>(st, g, bias_l0 + 256 * (2 * l), g0, h1, ws[2 * l]);
-                hidden_layer<kFP8, CB, KS_HID, kFP8>(st, g, bias_l0 + 256 * (2 * l + 1), g1, h0, ws[2 * l + 1]);
+                hidden_layer<kFP8, CB, KS_HID, kFP8, Q>(st, g, bias_l0 + 256 * (2 * l), g0, h1, ws[2 * l]);
+                hidden_layer<kFP8, CB, KS_HID, kFP8, Q>(st, g, bias_l0 + 256 * (2 * l + 1), g1, h0, ws[2 * l + 1]);
             }
-            hidden_layer<kFP8, CB, KS_HID, kFP8>(st, g, bias_l0 + 256 * 4, g0, h1, ws[4]);
-            hidden_layer<FP, CB, KS_HID, kFP8>(st, g, bias_l0 + 256 * 5, g1, h0, ws[5]);
+            hidden_layer<kFP8, CB, KS_HID, kFP8, Q>(st, g, bias_l0 + 256 * 4, g0, h1, ws[4]);
+            hidden_layer<FP, CB, KS_HID, kFP8, Q>(st, g, bias_l0 + 256 * 5, g1, h0, ws[5]);
         } else {
             for (int l = 0; l < 3; ++l) {
-                hidden_layer<PR, CB, KS_HID, PR>(st, g, bias_l0 + 256 * (2 * l), g0, h1);
-                hidden_layer<PR, CB, KS_HID, PR>(st, g, bias_l0 + 256 * (2 * l + 1), g1, h0);
+                hidden_layer<PR, CB, KS_HID, PR, Q>(st, g, bias_l0 + 256 * (2 * l), g0, h1);
+                hidden_layer<PR, CB, KS_HID, PR, Q>(st, g, bias_l0 + 256 * (2 * l + 1), g1, h0);
             }
         }
     };
+    static_assert(layer_chunks(PR, kHiddenL, 128) % 2 == 0, "hidden layers keep the slot parity");
     {
         auto gin = [&](auto K, auto C) { return din[CV(K)][CV(C)]; };
         hidden_layer<PR, CB, KS_D0, DIN == kDinEncoded ? FP : kF32>(st, g, BiasAt{bias_s, 0}, gin, h0);
     }
-    hidden6(BiasAt{bias_s, 256}, a.wscale + 1);
+    hidden6(std::integral_constant<int, 0>{}, BiasAt{bias_s, 256}, a.wscale + 1);
     // Head of the depth network: B / 64 passes of 64 classes (32 * kRbPerPass).
     const int npass = a.B / (32 * kRbPerPass);
     constexpr int PASS_FRAGS = KS_H * kRbPerPass;
@@ -974,16 +984,22 @@ render_kernel(const RenderArgs a) {
 #pragma unroll
             for (int ks = 0; ks < KS_S0; ++ks) sin_[ks][cb] = P::pack(f + E * ks);
         }
+        // Slot parity within a sample: its chunks add up to an even number,
+        // so every sample starts in slot 0.
+        constexpr int S0C = layer_chunks(PR, kSFirst, 128);
+        constexpr int HEADC = layer_chunks(PR, kSHead, 128);
+        constexpr int HIDC = 6 * layer_chunks(PR, kHiddenL, 128);
+        static_assert((S0C + HIDC + HEADC) % 2 == 0, "a sample's chunks keep the slot parity");
         {
             auto gs = [&](auto K, auto C) { return sin_[CV(K)][CV(C)]; };
-            hidden_layer<PR, CB, KS_S0, FP>(st, g, BiasAt{bias_s, s_bias}, gs, h0);
+            hidden_layer<PR, CB, KS_S0, FP, 0, layer_even_padded(kSFirst)>(st, g, BiasAt{bias_s, s_bias}, gs, h0);
         }
-        hidden6(BiasAt{bias_s, s_bias + 256}, a.wscale + 9);
+        hidden6(std::integral_constant<int, S0C & 1>{}, BiasAt{bias_s, s_bias + 256}, a.wscale + 9);
         auto gh = [&](auto K, auto C) {
             if constexpr (CV(K) < KS_H) return h0[CV(K)][CV(C)];
             else return skip[CV(K) - KS_H][CV(C)];
         };
-        run_pass<FP, CB, KS_H + KS_SK, 1, 0>(
+        run_pass<FP, CB, KS_H + KS_SK, 1, kChunkFrags * ((S0C + HIDC) & 1)>(
             st, g, BiasAt{bias_s, s_bias + 7 * 256}, gh, [&](auto R, auto C, const f32x16& acc) {
                 constexpr int cb = CV(C);
                 // lanes of group 0 hold rows 0..3 = (r, g, b, sigma) in registers 0..3
@@ -1000,8 +1016,6 @@ render_kernel(const RenderArgs a) {
                 Dp[cb] += wgt * tk[cb];
                 T[cb] *= exp_neg<FP == kF32>(tau);
             });
-        // the shading head is padded to an even number of chunks
-        if constexpr ((((KS_H + KS_SK) + kChunkFrags - 1) / kChunkFrags) & 1) st.template next<1>();
     }
     st.finish();  // no copy into LDS may outlive the workgroup
 
