@@ -31,7 +31,7 @@ HBM_PEAK_GBS = 8000.0
 # 256 MiB copy (FETCH_SIZE reads half the bytes moved: x2; WRITE_SIZE exact:
 # x1), per workload, valid only for the kernel sources they were taken with.
 MEASURED_TRAFFIC = {
-    "frame400_n4_bf16": {"sources_sha256_16": "d7d2c11a03d3a5e5", "fetch_kib": 7543.1 * 2, "write_kib": 11760.0},
+    "frame400_n4_bf16": {"sources_sha256_16": "8b04c2e0db155e03", "fetch_kib": 7284.5 * 2, "write_kib": 11760.0},
     "targets400_b128_k5_z5": {"sources_sha256_16": "41130f7b290df878", "fetch_kib": 9069.9 * 2, "write_kib": 400000.0},
 }
 # the sources (and the build script, whose flags shape the code) each
@@ -106,6 +106,8 @@ def log(msg):
 
 
 def cpu_baseline(wl, weights, poses, n_sample):
+    """The oracle on a seeded uniform sample of the workload's rays, timed on
+    this host; rays/s and the time per frame extrapolated from the sample."""
     from threadpoolctl import threadpool_info
 
     from oracle import donerf_oracle as O
@@ -118,10 +120,19 @@ def cpu_baseline(wl, weights, poses, n_sample):
              precision=wl.precision, select=wl.select, ray_subset=sub, depth_input=wl.depth_input)
     dt = time.perf_counter() - t0
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    return {"value": len(sub) / dt / 1e6, "unit": "Mrays/s", "cores": int(threads), "kind": "oracle",
+    rate = len(sub) / dt
+    return {"value": rate / 1e6, "unit": "Mrays/s", "cores": int(threads), "kind": "oracle",
+            "extrapolated": len(sub) < total,
+            "s_per_frame": round(wl.H * wl.W / rate, 2),
             "sample": f"{len(sub)} rays drawn uniformly (seed 1234) from the {wl.n_poses} x {wl.H} x "
-                      f"{wl.W} workload, {wl.precision}-rounding oracle, {dt:.1f} s; "
-                      f"os.cpu_count()={os.cpu_count()}"}
+                      f"{wl.W} workload, {wl.precision}-rounding oracle, {dt:.1f} s; the frame time is "
+                      f"extrapolated from it; os.cpu_count()={os.cpu_count()}"}
+
+
+def default_cpu_sample(wl):
+    """Rays of the oracle's timed sample: 262,144 for the 400 x 400 frames,
+    a 65,536-ray subset for the larger workloads (about 7-25 s each)."""
+    return 262144 if wl.H * wl.W <= 400 * 400 else 65536
 
 
 def mfma_loop_ceiling(r, precision, stream, workgroups=2048):
@@ -207,7 +218,9 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="frame400_n4_bf16")
-    ap.add_argument("--cpu-sample", type=int, default=262144)
+    ap.add_argument("--cpu-sample", type=int, default=None,
+                    help="rays of the oracle's timed sample (default: 262,144 for 400 x 400 frames, "
+                         "65,536 for larger workloads)")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-mfma-loop", action="store_true",
                     help="skip the register-fed MFMA loop that measures the matrix cores' ceiling")
@@ -298,6 +311,8 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4),
         "ms_per_frame": round(ms_step / P, 4),
+        **({"ms_per_stereo_pair": round(ms_step / (P // 2), 4),
+            "stereo_pairs_per_s": round((P // 2) / (ms_step * 1e-3), 3)} if wl.stereo else {}),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": round(value / paper_mrays, 2) if wl.name == "frame400_n4_bf16" else None,
@@ -327,7 +342,7 @@ def main():
         if wl.precision != "fp8":   # the fp8 network mixes fp8 and bf16 layers
             line["roofline"]["frac_of_mfma_loop"] = round(achieved / loop, 4)
     if not args.no_cpu:
-        line["cpu_baseline"] = cpu_baseline(wl, weights, poses, args.cpu_sample)
+        line["cpu_baseline"] = cpu_baseline(wl, weights, poses, args.cpu_sample or default_cpu_sample(wl))
     r.close()
     print(json.dumps(line), flush=True)
 
