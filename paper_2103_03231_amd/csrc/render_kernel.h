@@ -132,6 +132,15 @@ constexpr int kChunkVec = kChunkBytes / 16;  // u32x4 per chunk
 #endif
 constexpr int kFragAhead = DONERF_FRAG_AHEAD;
 constexpr int kFragAheadFp8 = DONERF_FRAG_AHEAD_FP8;
+#ifndef DONERF_FP8_OVERLAP
+#define DONERF_FP8_OVERLAP 1
+#endif
+#ifndef DONERF_FP8_EPI_DELAY
+#define DONERF_FP8_EPI_DELAY 2
+#endif
+#ifndef DONERF_FP8_BIAS_LEAD
+#define DONERF_FP8_BIAS_LEAD 3
+#endif
 
 // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
 template <int VM>
@@ -345,6 +354,14 @@ __device__ __forceinline__ void hidden_layer(WS& st, int g, BiasAt bias, GetB&& 
     static_assert(OUT != kFP8 || RBP == 2, "an fp8 K step takes two row blocks");
     f32x16 acc[2][RBP][CB];
     u32x4 a[D + 1][U];
+    constexpr int NP = 8 / RBP;        // passes
+    // Overlapped passes (fp8 steps): the next pass's biases are read into its
+    // accumulator set LEAD steps before the current pass ends, and a pass's
+    // epilogue runs DEL steps into the next pass.
+    constexpr bool OV = DONERF_FP8_OVERLAP && MP == kFP8;
+    constexpr int DEL = DONERF_FP8_EPI_DELAY < PF - 2 ? DONERF_FP8_EPI_DELAY : PF - 2;
+    constexpr int LEAD = DONERF_FP8_BIAS_LEAD < PF - DEL - 1 ? DONERF_FP8_BIAS_LEAD : PF - DEL - 1;
+    static_assert(!OV || LEAD >= 1, "overlap needs room between the epilogue and the next biases");
     auto load_bias = [&](auto PP) {
         constexpr int q = CV(PP);
         sfor<RBP>([&](auto R) {
@@ -393,13 +410,23 @@ __device__ __forceinline__ void hidden_layer(WS& st, int g, BiasAt bias, GetB&& 
         if constexpr (s >= D) {
             constexpr int f = s - D;
             constexpr int p = f / PF, w = f % PF, k = w / RBP, r = w % RBP;
-            if constexpr (w == 0) load_bias(std::integral_constant<int, p>{});
+            if constexpr (!OV) {
+                if constexpr (w == 0) load_bias(std::integral_constant<int, p>{});
+            } else {
+                if constexpr (p == 0 && w == 0) load_bias(std::integral_constant<int, 0>{});
+                if constexpr (p + 1 < NP && w == PF - LEAD) load_bias(std::integral_constant<int, p + 1>{});
+            }
             sfor<CB>([&](auto C) {
                 u32x4 bk[U];
                 sfor<U>([&](auto V) { bk[CV(V)] = getB(std::integral_constant<int, k * U + CV(V)>{}, C); });
                 acc[p & 1][r][CV(C)] = M::mma(a[f % (D + 1)], bk, acc[p & 1][r][CV(C)], sa);
             });
-            if constexpr (w == PF - 1) epilogue(std::integral_constant<int, p>{});
+            if constexpr (!OV) {
+                if constexpr (w == PF - 1) epilogue(std::integral_constant<int, p>{});
+            } else {
+                if constexpr (p >= 1 && w == DEL) epilogue(std::integral_constant<int, p - 1>{});
+                if constexpr (p == NP - 1 && w == PF - 1) epilogue(std::integral_constant<int, p>{});
+            }
         }
         __builtin_amdgcn_sched_barrier(0x6);
     });
