@@ -42,6 +42,10 @@ KERNEL_SOURCES = {
                          "paper_2103_03231_amd/build.py"),
     "targets400_b128_k5_z5": ("paper_2103_03231_amd/csrc/targets.hip", "paper_2103_03231_amd/csrc/internal.h",
                               "paper_2103_03231_amd/build.py"),
+    "stereo1440x1600_n16_b256_cdf_bf16": ("paper_2103_03231_amd/csrc/render_kernel.h",
+                                          "paper_2103_03231_amd/csrc/render_bf16_cdf_wide.hip",
+                                          "paper_2103_03231_amd/csrc/layout.h", "paper_2103_03231_amd/csrc/internal.h",
+                                          "paper_2103_03231_amd/build.py"),
 }
 
 
@@ -93,10 +97,12 @@ def mixed_peak(N: int, n_bins: int, d_in: int) -> float:
     return tot / t
 
 
-def padded_flop_per_ray(N: int, n_bins: int, d_in: int = 90) -> int:
+def padded_flop_per_ray(N: int, n_bins: int, d_in: int = 90, head_sweeps: int = 1) -> int:
     """2 x multiply-adds the MFMA tiles execute (K padded to 96 (16 for the
-    folded positions layer) / 64 / 288, shading head padded to 32 rows)."""
-    d = (96 if d_in == 90 else 16) * 256 + 6 * 256 * 256 + 256 * n_bins
+    folded positions layer) / 64 / 288, shading head padded to 32 rows; the
+    depth head twice where inverse-CDF placement over more than 128 classes
+    runs it in two sweeps)."""
+    d = (96 if d_in == 90 else 16) * 256 + 6 * 256 * 256 + head_sweeps * 256 * n_bins
     s = 64 * 256 + 6 * 256 * 256 + 288 * 32
     return 2 * (d + N * s)
 
@@ -293,6 +299,7 @@ def main():
     ms_step = wall * 1e3 / args.steps
     value = rays / (ms_step * 1e-3) / 1e6
     d_in = depth_in_folded(wl.depth_input)
+    sweeps = 2 if wl.select == "cdf" and wl.n_bins > 128 else 1
     flop_launch = algorithmic_flop_per_ray(wl.N, wl.n_bins, d_in) * rays
     achieved = flop_launch / (avg_kern_ms * 1e-3) / 1e12
     peak = (mixed_peak(wl.N, wl.n_bins, d_in) if wl.precision == "fp8" else MFMA_PEAK_TFLOPS[wl.precision])
@@ -323,11 +330,11 @@ def main():
                    "depth_classes": wl.n_bins, "placement": wl.select, "depth_input": wl.depth_input,
                    "rays_per_step": rays,
                    "algorithmic_mflop_per_ray": round(algorithmic_flop_per_ray(wl.N, wl.n_bins, d_in) / 1e6, 4),
-                   "padded_mflop_per_ray": round(padded_flop_per_ray(wl.N, wl.n_bins, d_in) / 1e6, 4)},
+                   "padded_mflop_per_ray": round(padded_flop_per_ray(wl.N, wl.n_bins, d_in, sweeps) / 1e6, 4)},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(achieved / peak, 4),
                      # the same launch counted by the tile work the MFMAs execute (padding included)
-                     "padded_frac": round(padded_flop_per_ray(wl.N, wl.n_bins, d_in) * rays
+                     "padded_frac": round(padded_flop_per_ray(wl.N, wl.n_bins, d_in, sweeps) * rays
                                           / (avg_kern_ms * 1e-3) / 1e12 / peak, 4),
                      **({"peak_note": "fp8 hidden layers at 5000, bf16 first layers and heads at 2500, "
                                       "combined by their share of the work"} if wl.precision == "fp8" else {}),

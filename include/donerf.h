@@ -84,7 +84,9 @@ typedef enum donerf_select {
                                        coordinate of Eq. 3), its CDF inverted at
                                        u_i = (i + 0.5)/N; sample i's width is the
                                        depth extent of the slice [i/N, (i+1)/N].
-                                       fp32 arithmetic; n_bins <= 128          */
+                                       fp32 arithmetic; above 128 classes the
+                                       depth head runs twice (class sums, then
+                                       the values the targets fall in)       */
 } donerf_select;
 
 typedef enum donerf_depth_input {
@@ -146,7 +148,7 @@ size_t donerf_weight_count(int32_t n_bins, int32_t depth_input);
  *             on return
  *   out       receives the handle; set to NULL on failure
  * Errors: E_INVALID_ARG (NULL, cfg ranges), E_UNSUPPORTED (n_bins not in the
- * supported set, or above 128 with DONERF_SELECT_CDF), E_SIZE (n_weights !=
+ * supported set), E_SIZE (n_weights !=
  * donerf_weight_count(cfg->n_bins, cfg->depth_input)),
  * E_NONFINITE (NaN/Inf in cfg or weights), E_DEVICE (no device or not
  * gfx950), E_NOMEM, E_HIP.

@@ -30,6 +30,7 @@ COMMON = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-ffp-contract=
 UNIT_FLAGS = {
     "render_bf16_topn.hip": ["-mllvm", "-amdgpu-sched-strategy=iterative-ilp"],
     "render_bf16_cdf.hip": ["-mllvm", "-amdgpu-sched-strategy=iterative-ilp"],
+    "render_bf16_cdf_wide.hip": ["-mllvm", "-amdgpu-sched-strategy=iterative-ilp"],
 }
 
 

@@ -62,6 +62,10 @@ size_t blob_w_count(int l, int n_bins, int depth_input) {
 
 bool bins_supported(int B) { return B >= 64 && B <= 256 && B % 64 == 0; }
 
+// Inverse-CDF placement over more classes than fit in registers: the kernel
+// runs the depth head twice, and the depth stream carries its chunks twice.
+bool wide_cdf(const donerf_cfg& c) { return c.select == DONERF_SELECT_CDF && c.n_bins > 128; }
+
 int validate_cfg(const donerf_cfg* c) {
     if (!c) return fail(DONERF_E_INVALID_ARG, "cfg is NULL");
     const float fs[] = {c->near_dist, c->far_dist, c->fov_x_deg, c->centre[0], c->centre[1],
@@ -86,8 +90,6 @@ int validate_cfg(const donerf_cfg* c) {
         return fail(DONERF_E_INVALID_ARG, "unknown depth_input");
     if (!bins_supported(c->n_bins))
         return fail(DONERF_E_UNSUPPORTED, "n_bins must be 64, 128, 192 or 256");
-    if (c->select == DONERF_SELECT_CDF && c->n_bins > 128)
-        return fail(DONERF_E_UNSUPPORTED, "inverse-CDF placement supports n_bins 64 and 128");
     return DONERF_OK;
 }
 
@@ -338,6 +340,11 @@ int render_impl(donerf_t* h, const float* poses, int32_t P, int32_t H, int32_t W
     a.H = H;
     a.W = W;
     a.N = N;
+    static_assert(kMaxSamples == DONERF_MAX_SAMPLES, "sample capacity");
+    for (int i = 0; i < kMaxSamples; ++i) {
+        a.cdf_u[i] = i < N ? ((float)i + 0.5f) / (float)N : 2.0f;
+        a.cdf_u[kMaxSamples + i] = i + 1 < N ? (float)(i + 1) / (float)N : 2.0f;
+    }
     a.B = c.n_bins;
     a.focal = (float)((0.5 * W) / std::tan((double)c.fov_x_deg * (M_PI / 180.0) * 0.5));
     a.half_w = 0.5f * (float)W;
@@ -349,7 +356,7 @@ int render_impl(donerf_t* h, const float* poses, int32_t P, int32_t H, int32_t W
     a.near = c.near_dist;
     a.dmax = c.far_dist;
     a.log2_span1 = (float)std::log2((double)c.far_dist - (double)c.near_dist + 1.0);
-    const int place = c.select == DONERF_SELECT_CDF ? 1 : 0;
+    const int place = c.select != DONERF_SELECT_CDF ? kPlaceTopN : wide_cdf(c) ? kPlaceCdfWide : kPlaceCdf;
     for (int32_t p0 = 0; p0 < P; p0 += kMaxPosesPerLaunch) {
         const int np = P - p0 < kMaxPosesPerLaunch ? P - p0 : kMaxPosesPerLaunch;
         a.n_poses = np;
@@ -436,6 +443,10 @@ int donerf_create(const donerf_cfg* cfg, const float* weights, size_t n_weights,
             pack_layer(fp, prec, kind, B, weights + off, s, frags);
         }
         (l < 8 ? n_d_chunks : n_s_chunks) += layer_chunks(prec, kind, B);
+        if (l == 7 && wide_cdf(*cfg)) {
+            pack_layer(fp, prec, kind, B, weights + off, s, frags);
+            n_d_chunks += layer_chunks(prec, kind, B);
+        }
         off += blob_w_count(l, B, cfg->depth_input);
         // the depth head's bias (B-dependent length) goes last
         std::vector<float>& dst = l == 7 ? head_bias : bias;

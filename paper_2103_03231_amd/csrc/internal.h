@@ -9,6 +9,8 @@
 
 namespace donerf {
 
+constexpr int kMaxSamples = 16;   // samples per ray (include/donerf.h DONERF_MAX_SAMPLES)
+
 // Everything one render launch needs, passed by value as the kernel argument.
 struct RenderArgs {
     const uint4* d_frags;   // depth network fragments, chunk-padded per layer
@@ -40,6 +42,11 @@ struct RenderArgs {
     float near;             // d_min
     float dmax;             // d_max
     float log2_span1;       // log2(d_max - d_min + 1), for the inverse of Eq. 3
+    // inverse-CDF targets (Sec. 5.1): cdf_u[i] = (i + 1/2) / N, the centre of
+    // probability slice i < N, and cdf_u[kMaxSamples + i] = (i + 1) / N, the
+    // inner end of slice i < N - 1; 2 elsewhere.  Each is the correctly
+    // rounded fp32 quotient, as the kernel's own division would give.
+    float cdf_u[2 * kMaxSamples];
     int32_t wscale[16];     // per streamed layer (depth 0-7, shading 8-15): E8M0 scale of
                             // its fp8 weights, 127 - s for weights stored as W 2^s
     float poses[kMaxPosesPerLaunch][12];
@@ -75,6 +82,9 @@ hipError_t launch_render_fp32_topn(int ncap, int din, const RenderArgs& a, dim3 
 hipError_t launch_render_fp32_cdf(int ncap, int din, const RenderArgs& a, dim3 grid, hipStream_t stream);
 hipError_t launch_render_fp8_topn(int ncap, int din, const RenderArgs& a, dim3 grid, hipStream_t stream);
 hipError_t launch_render_fp8_cdf(int ncap, int din, const RenderArgs& a, dim3 grid, hipStream_t stream);
+hipError_t launch_render_bf16_cdf_wide(int ncap, int din, const RenderArgs& a, dim3 grid, hipStream_t stream);
+hipError_t launch_render_fp32_cdf_wide(int ncap, int din, const RenderArgs& a, dim3 grid, hipStream_t stream);
+hipError_t launch_render_fp8_cdf_wide(int ncap, int din, const RenderArgs& a, dim3 grid, hipStream_t stream);
 // Composites the split parts of rays [n_full * rays_per_block, total_rays)
 // into out_rgb / out_depth.
 hipError_t launch_combine(int prec, const RenderArgs& a, hipStream_t stream);

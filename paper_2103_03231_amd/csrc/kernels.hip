@@ -81,6 +81,10 @@ __global__ void __launch_bounds__(256) topn_kernel(const float* scores, int32_t 
 hipError_t launch_render(int prec, int ncap, int place, int din, const RenderArgs& a, uint32_t n_split_tiles,
                          hipStream_t stream) {
     const dim3 grid(a.n_full + n_split_tiles * (uint32_t)a.split);
+    if (place == kPlaceCdfWide)
+        return prec == kFP8    ? launch_render_fp8_cdf_wide(ncap, din, a, grid, stream)
+               : prec == kBF16 ? launch_render_bf16_cdf_wide(ncap, din, a, grid, stream)
+                               : launch_render_fp32_cdf_wide(ncap, din, a, grid, stream);
     if (prec == kFP8)
         return place == kPlaceCdf ? launch_render_fp8_cdf(ncap, din, a, grid, stream)
                                   : launch_render_fp8_topn(ncap, din, a, grid, stream);

@@ -127,8 +127,11 @@ DN_HD constexpr int p_feature(int ks, int g, int e) {
     return 8 * ks + 2 * e + g < kPIn ? 8 * ks + 2 * e + g : -1;
 }
 
-// Sample placement and depth-network input of a render variant.
-enum Placement { kPlaceTopN = 0, kPlaceCdf = 1 };
+// Sample placement and depth-network input of a render variant.  kPlaceCdf
+// keeps a ray's B <= 128 class values in registers; kPlaceCdfWide (B = 192,
+// 256) runs the depth head twice, so the depth stream of such a network
+// carries the head's chunks twice.
+enum Placement { kPlaceTopN = 0, kPlaceCdf = 1, kPlaceCdfWide = 2 };
 enum DepthInput { kDinEncoded = 0, kDinPositions = 1 };
 
 // Layer roles in the streamed weight sequence.  kDFirstPos is the folded

@@ -119,6 +119,14 @@ __device__ __forceinline__ void lds_barrier() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
+// Orders one wave's LDS accesses across its lanes: LDS executes a wave's
+// instructions in order, so only the compiler has to keep them in place.
+__device__ __forceinline__ void wave_lds_fence() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+}
+
 constexpr int kChunkVec = kChunkBytes / 16;  // u32x4 per chunk
 // LDS fragment reads in flight, in MFMA steps: bf16 and fp32 steps read
 // one 1 KiB unit, fp8 steps two.  Measured on 5 x 400 x 400, N = 4: 12 bf16
@@ -246,12 +254,12 @@ __device__ __forceinline__ f32x16 bias_frag(BiasAt bias, int g) {
 // One accumulator pass: RBP output row blocks x CB column blocks over KS K
 // steps.  BASE is the index of the pass's first fragment within its layer;
 // layers start on chunk boundaries, so chunk changes are known statically.
-template <int PR, int CB, int KS, int RBP, int BASE, class WS, class GetB, class Epi>
+// D: LDS reads issued this many fragments ahead.
+template <int PR, int CB, int KS, int RBP, int BASE, int D = kFragAhead, class WS, class GetB, class Epi>
 __device__ __forceinline__ void run_pass(WS& st, int g, BiasAt bias, GetB& getB, Epi&& epi) {
     using P = Prec<PR>;
     static_assert(P::U == 1, "heads run single-unit steps");
     constexpr int NF = KS * RBP;   // fragments of the pass, in (K step, row block) order
-    constexpr int D = kFragAhead;  // LDS reads issued this many fragments ahead
     f32x16 acc[RBP][CB];
     sfor<RBP>([&](auto R) {
         const f32x16 b = bias_frag(bias + 32 * CV(R), g);
@@ -541,7 +549,7 @@ __device__ __forceinline__ float pick_f(const float* v, int n, int k) {
 // that owns it.  Everything is fp32.
 template <int NPM, int NCAP>
 __device__ __forceinline__ void cdf_place(const float (&v)[NPM][kRbPerPass][16], int g, int N, int B,
-                                          float near, float far, float log2_span1, float (&ts)[NCAP],
+                                          const float* u, float near, float far, float log2_span1, float (&ts)[NCAP],
                                           float (&ds)[NCAP], int (&cls)[NCAP]) {
     constexpr int NLB = NPM * kRbPerPass * 4;  // lane-local blocks
     constexpr int NB = 2 * NLB;                // blocks in class order
@@ -608,10 +616,10 @@ __device__ __forceinline__ void cdf_place(const float (&v)[NPM][kRbPerPass][16],
     for (int i = 0; i < NCAP; ++i) {
         if (i < N) {
             int k;
-            ts[i] = to_depth(inverse(((float)i + 0.5f) / (float)N, k));
+            ts[i] = to_depth(inverse(u[i], k));
             cls[i] = k;
             int kk;
-            edge[i + 1] = i + 1 < N ? to_depth(inverse((float)(i + 1) / (float)N, kk)) : far;
+            edge[i + 1] = i + 1 < N ? to_depth(inverse(u[kMaxSamples + i], kk)) : far;
         } else {
             ts[i] = far;
             cls[i] = B - 1;
@@ -743,6 +751,19 @@ __device__ __forceinline__ float one_minus_exp_neg(float x) {
 constexpr int kDepthHeadBias = 7 * 256 + 7 * 256 + 32;
 constexpr int kBiasMax = kDepthHeadBias + 256;
 
+// LDS table of the wide inverse-CDF placement, one region per wave: first a
+// ray's prefix over its 64 4-class blocks (stride 65 floats, odd so that the
+// rays of a wave spread over the banks), later one head pass's class values
+// (8 x 64 lanes x 16 bytes).
+#ifndef DONERF_CDFW_AHEAD
+#define DONERF_CDFW_AHEAD 4
+#endif
+constexpr int kCdfRayStride = 65;
+constexpr int kCdfWaveFloats = 32 * kCdfRayStride;
+constexpr int kCdfClass = 2 * 16;   // a ray's sample classes follow its (depth, width) pairs
+static_assert(kCdfClass + 16 <= kCdfRayStride, "a ray's samples fit its row");
+static_assert(kCdfWaveFloats >= 8 * 64 * 4 && kCdfWaveFloats % 4 == 0, "a pass's values fit a wave's region");
+
 // PR: network precision (layout.h Precision; an fp8 network keeps its first
 // layers and heads in bf16).  CB: 32-ray column blocks per wave.  NW: waves
 // per workgroup.  OCC: waves per SIMD the register budget is sized for (with
@@ -767,6 +788,7 @@ render_kernel(const RenderArgs a) {
     __shared__ u32x4 ring1[kChunkVec];
     __shared__ float bias_s[kBiasMax];
     __shared__ float bins_s[2 * 256];
+    __shared__ __align__(16) float cdf_s[PLACE == kPlaceCdfWide ? NW * kCdfWaveFloats : 4];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -943,7 +965,7 @@ render_kernel(const RenderArgs a) {
             top[CV(C)].merge_partner();
             top[CV(C)].ascending(a.N, sel[CV(C)]);
         });
-    } else {
+    } else if constexpr (PLACE == kPlaceCdf) {
         // Inverse-CDF placement needs every class value of the ray; B <= 128
         // keeps them in registers (the hidden activations h1 are dead here).
         static_assert(PASS_FRAGS % kChunkFrags == 0, "a pass spans whole chunks");
@@ -970,9 +992,164 @@ render_kernel(const RenderArgs a) {
             }
         });
         sfor<CB>([&](auto C) {
-            cdf_place<NPM, NCAP>(vals[CV(C)], g, a.N, a.B, a.near, a.dmax, a.log2_span1, st_t[CV(C)],
+            cdf_place<NPM, NCAP>(vals[CV(C)], g, a.N, a.B, a.cdf_u, a.near, a.dmax, a.log2_span1, st_t[CV(C)],
                                  st_d[CV(C)], sel[CV(C)]);
         });
+    } else {
+        // Inverse-CDF placement for B = 192 and 256, whose class values do
+        // not fit in registers.  The steps are cdf_place's: 4-class block
+        // sums, their prefix in class order, a target u located by that
+        // prefix, then inside its block.
+        //   sweep 1: the head's passes yield the block sums only; the ray's
+        //            prefix goes to its row of the wave's LDS table, and each
+        //            target's block b and its rest r = m - pre[b] come from a
+        //            binary search of that row;
+        //   sweep 2: the head runs again (the depth stream carries its
+        //            chunks twice); each pass stages its class values in the
+        //            table, and every target whose block lies in the pass
+        //            reads that block's four values and is resolved.
+        // Both lane groups of a ray compute the same targets.
+        static_assert(CB == 1, "the LDS table holds one 32-ray column block per wave");
+        static_assert(PASS_FRAGS % kChunkFrags == 0, "a pass spans whole chunks");
+        constexpr int NPM = 256 / (32 * kRbPerPass);   // passes at B = 256
+        constexpr int NLB = NPM * kRbPerPass * 4;      // lane-local blocks
+        constexpr int NB = 2 * NLB;                    // blocks in class order
+        constexpr int NT = 2 * NCAP - 1;               // targets: NCAP slice centres, NCAP - 1 inner slice ends
+        static_assert(NB <= kCdfRayStride && NB == 64, "a ray's prefix fits its row; 4 bits of block per pass");
+        const int tbase = wave * kCdfWaveFloats;
+        const int rbase = tbase + col * kCdfRayStride;
+        auto target_u = [&](int t) { return t < NCAP ? a.cdf_u[t] : a.cdf_u[kMaxSamples + t - NCAP]; };
+        auto head_pass = [&](auto PI, auto&& epi) {
+            constexpr int p = CV(PI);
+            run_pass<FP, CB, KS_H, kRbPerPass, p * PASS_FRAGS, DONERF_CDFW_AHEAD>(
+                st, g, BiasAt{bias_s, kDepthHeadBias + 32 * kRbPerPass * p}, g0, epi);
+        };
+
+        // sweep 1: block sums (absent passes of B = 192 add zeros)
+        float bs[NLB];
+        sfor<NPM>([&](auto PI) {
+            constexpr int p = CV(PI);
+            if (p < npass) {
+                head_pass(PI, [&](auto R, auto C, const f32x16& acc) {
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const float v0 = sigmoid<FP == kF32>(acc[4 * q]), v1 = sigmoid<FP == kF32>(acc[4 * q + 1]);
+                        const float v2 = sigmoid<FP == kF32>(acc[4 * q + 2]), v3 = sigmoid<FP == kF32>(acc[4 * q + 3]);
+                        bs[(p * kRbPerPass + CV(R)) * 4 + q] = ((v0 + v1) + v2) + v3;
+                    }
+                    dump_scores(p, CV(R), CV(C), acc);
+                });
+            } else {
+                if constexpr (CPP == 1 && (p & 1)) st.template next<1>();   // padding chunk
+#pragma unroll
+                for (int i = 0; i < kRbPerPass * 4; ++i) bs[p * kRbPerPass * 4 + i] = 0.0f;
+            }
+        });
+        // prefix pre[b] (the blocks before b) in class order: block b lies
+        // on lane group b & 1, lane-local block b >> 1; group g stores the
+        // entries of parity g
+        float total;
+        {
+            float pre = 0.0f;
+#pragma unroll
+            for (int b2 = 0; b2 < NB; b2 += 2) {
+                const float own = bs[b2 >> 1];
+                const float other = __shfl_xor(own, 32);
+                const float e0 = g ? other : own;   // block b2 (group 0)
+                const float e1 = g ? own : other;   // block b2 + 1 (group 1)
+                const float pre1 = pre + e0;
+                cdf_s[rbase + b2 + g] = g ? pre1 : pre;
+                pre = pre1 + e1;
+            }
+            total = pre;
+        }
+        wave_lds_fence();
+        // Block b of target t: the last with pre[b] <= m (pre[0] = 0), which
+        // is cdf_place's count of block ends at or below m (m < total, so
+        // b < B / 4).
+        // Per target one byte holds 4 b, later 4 b + j = its class.
+        uint32_t tk[(NT + 3) / 4];
+        float tr[NT];
+#pragma unroll
+        for (int i = 0; i < (NT + 3) / 4; ++i) tk[i] = 0;
+        sfor<NT>([&](auto T) {
+            constexpr int t = CV(T);
+            const float m = target_u(t) * total;
+            int b = 0;
+            float lo = 0.0f;
+#pragma unroll
+            for (int step = NB / 2; step >= 1; step >>= 1) {
+                const float v = cdf_s[rbase + b + step];
+                const bool take = v <= m;
+                b = take ? b + step : b;
+                lo = take ? v : lo;
+            }
+            tk[t / 4] |= (uint32_t)(4 * b) << (8 * (t % 4));
+            tr[t] = m - lo;
+            // four searches at a time: the scheduler would otherwise
+            // interleave all of them and hold every step's compare mask
+            if constexpr (t % 4 == 3) __builtin_amdgcn_sched_barrier(0);
+        });
+
+        // sweep 2: resolve each target in its block's pass; tr then holds
+        // its coordinate s
+        const float inv_b = 1.0f / (float)a.B;
+        sfor<NPM>([&](auto PI) {
+            constexpr int p = CV(PI);
+            if (p < npass) {
+                wave_lds_fence();   // the table's earlier reads come before these writes
+                head_pass(PI, [&](auto R, auto C, const f32x16& acc) {
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        f32x4 v;
+                        v[0] = sigmoid<FP == kF32>(acc[4 * q]);
+                        v[1] = sigmoid<FP == kF32>(acc[4 * q + 1]);
+                        v[2] = sigmoid<FP == kF32>(acc[4 * q + 2]);
+                        v[3] = sigmoid<FP == kF32>(acc[4 * q + 3]);
+                        *reinterpret_cast<f32x4*>(&cdf_s[tbase + 4 * ((CV(R) * 4 + q) * 64 + lane)]) = v;
+                    }
+                });
+                wave_lds_fence();
+                sfor<NT>([&](auto T) {
+                    constexpr int t = CV(T);
+                    const int kb = (int)(tk[t / 4] >> (8 * (t % 4))) & 255;
+                    if ((kb >> 6) == p) {   // the block's pass (a resolved target keeps it)
+                        // block b = 16 p + 8 R + 2 q + g': values of lane col + 32 g'
+                        const int b = kb >> 2;
+                        const int slot = (((b >> 3) & 1) * 4 + ((b >> 1) & 3)) * 64 + col + 32 * (b & 1);
+                        const f32x4 w = *reinterpret_cast<const f32x4*>(&cdf_s[tbase + 4 * slot]);
+                        const float r = tr[t];
+                        const float c1 = w[0], c2 = c1 + w[1], c3 = c2 + w[2];
+                        const int j = (r >= c1 ? 1 : 0) + (r >= c2 ? 1 : 0) + (r >= c3 ? 1 : 0);
+                        const float base = j == 0 ? 0.0f : j == 1 ? c1 : j == 2 ? c2 : c3;
+                        const float aj = j == 0 ? w[0] : j == 1 ? w[1] : j == 2 ? w[2] : w[3];
+                        const float frac =
+                            aj > 0.0f ? fminf(fmaxf((r - base) * __builtin_amdgcn_rcpf(aj), 0.0f), 1.0f) : 0.0f;
+                        tr[t] = ((float)(4 * b + j) + frac) * inv_b;
+                        tk[t / 4] += (uint32_t)j << (8 * (t % 4));
+                    }
+                });
+            } else {
+                if constexpr (CPP == 1 && (p & 1)) st.template next<1>();   // padding chunk
+            }
+        });
+        // The ray's samples go to its row (depth, width at 2 k, 2 k + 1; class
+        // at kCdfClass + k), where the shading loop reads them: held in
+        // registers through that loop they would spill.
+        wave_lds_fence();   // the staged values are read
+        auto to_depth = [&](float s) { return a.near + exp2f(s * a.log2_span1) - 1.0f; };  // inverse of Eq. 3
+        float lo_edge = a.near;
+#pragma unroll
+        for (int i = 0; i < NCAP; ++i) {
+            if (i < a.N) {
+                // (the last centre has no inner end after it: N <= NCAP)
+                const float hi_edge = i + 1 < a.N ? to_depth(tr[NCAP + (i + 1 < NCAP ? i : 0)]) : a.dmax;
+                cdf_s[rbase + 2 * i + g] = g ? hi_edge - lo_edge : to_depth(tr[i]);
+                cdf_s[rbase + kCdfClass + i] = __int_as_float((int)(tk[i / 4] >> (8 * (i % 4))) & 255);
+                lo_edge = hi_edge;
+            }
+        }
+        wave_lds_fence();
     }
     // sample k of column block cb: depth, width
     auto sample_td = [&](int cb, int k, float& t, float& d) {
@@ -982,9 +1159,13 @@ render_kernel(const RenderArgs a) {
             const int bin = min(pick(sel[cb], k), a.B - 1);
             t = bins_s[bin];
             d = bins_s[a.B + bin];
-        } else {
+        } else if constexpr (PLACE == kPlaceCdf) {
             t = pick_f(st_t[cb], NCAP, k);
             d = pick_f(st_d[cb], NCAP, k);
+        } else {
+            const int row = wave * kCdfWaveFloats + col * kCdfRayStride;
+            t = cdf_s[row + 2 * k];
+            d = cdf_s[row + 2 * k + 1];
         }
     };
 
@@ -1066,7 +1247,13 @@ render_kernel(const RenderArgs a) {
                 if (a.out_depth) a.out_depth[rid[cb]] = Dp[cb];
             }
             if (a.out_bins && part == 0) {
-                for (int k = 0; k < a.N; ++k) a.out_bins[(size_t)rid[cb] * a.N + k] = pick(sel[cb], k);
+                for (int k = 0; k < a.N; ++k) {
+                    if constexpr (PLACE == kPlaceCdfWide)
+                        a.out_bins[(size_t)rid[cb] * a.N + k] =
+                            __float_as_int(cdf_s[wave * kCdfWaveFloats + col * kCdfRayStride + kCdfClass + k]);
+                    else
+                        a.out_bins[(size_t)rid[cb] * a.N + k] = pick(sel[cb], k);
+                }
             }
             if (a.out_samples && part == 0) {
                 for (int k = 0; k < a.N; ++k) {

@@ -256,6 +256,8 @@ WORKLOADS = {
                                        fov_deg=90.0, select="topn_softmax"),
     "stereo1440x1600_n16_b256_bf16": Workload("stereo1440x1600_n16_b256_bf16", 1600, 1440,
                                               tuple(range(60)), 16, n_bins=256, stereo=True),
+    "stereo1440x1600_n16_b256_cdf_bf16": Workload("stereo1440x1600_n16_b256_cdf_bf16", 1600, 1440,
+                                                  tuple(range(60)), 16, n_bins=256, stereo=True, select="cdf"),
 }
 
 

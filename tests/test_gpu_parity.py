@@ -508,6 +508,11 @@ def check_cdf(g, w, poses, H, W, N, precision, n_bins=128, subset=None, label=""
     (2, 64, 37, 29, 1),
     (8, 128, 16, 24, 2),
     (16, 128, 12, 20, 1),
+    # 192 and 256 classes: the two-sweep placement
+    (4, 256, 24, 40, 1),
+    (16, 256, 12, 20, 2),
+    (8, 192, 16, 24, 2),
+    (1, 192, 17, 23, 1),
 ])
 def test_cdf_placement(precision, N, B, H, W, P):
     r, w = renderer(precision, n_bins=B, n_max=max(N, 4), select=b.SELECT_CDF)
@@ -515,12 +520,6 @@ def test_cdf_placement(precision, N, B, H, W, P):
     g = gpu_render(r, poses, H, W, N)
     check_cdf(g, w, poses, H, W, N, precision, n_bins=B, label=f"cdf {precision} N={N} B={B} {P}x{H}x{W}")
     r.close()
-
-
-def test_cdf_rejects_256_classes():
-    with pytest.raises(b.DonerfError) as e:
-        renderer("bf16", n_bins=256, select=b.SELECT_CDF)
-    assert e.value.status == b.E_UNSUPPORTED
 
 
 def test_frame400_n4_cdf_bf16_sampled():
@@ -531,6 +530,20 @@ def test_frame400_n4_cdf_bf16_sampled():
     g = _render_subset(r, wl, poses, subset)
     r.close()
     check_cdf(g, w, poses, wl.H, wl.W, wl.N, wl.precision, subset=subset, label=wl.name)
+
+
+def test_stereo_cdf_b256_sampled():
+    """The two-sweep placement at the headset shape: one stereo pair of
+    1440 x 1600 views, N = 16, 256 classes, rendered whole in the bench's
+    launch shape, checked on sampled rays."""
+    wl = inputs.WORKLOADS["stereo1440x1600_n16_b256_cdf_bf16"]
+    r, w = renderer(wl.precision, n_bins=wl.n_bins, n_max=wl.N, select=b.SELECT_CDF)
+    poses = wl.poses()[:2]
+    total = len(poses) * wl.H * wl.W
+    subset = np.unique(np.concatenate([np.random.default_rng(4).integers(0, total, 600), [0, total - 1]]))
+    g = _render_subset(r, wl, poses, subset)
+    r.close()
+    check_cdf(g, w, poses, wl.H, wl.W, wl.N, wl.precision, n_bins=wl.n_bins, subset=subset, label=wl.name)
 
 
 # ------------------------------------------------------------------ depth-network input features
@@ -649,6 +662,7 @@ def test_positions_inputs_match_oracle(B):
     (8, 256, 16, 24, 1, "topn"),
     (16, 192, 12, 20, 2, "topn"),
     (4, 128, 24, 40, 1, "cdf"),
+    (4, 256, 24, 40, 1, "cdf"),
 ])
 def test_positions_variants(precision, N, B, H, W, P, select):
     sel = b.SELECT_CDF if select == "cdf" else b.SELECT_TOPN
@@ -674,6 +688,8 @@ def test_positions_variants(precision, N, B, H, W, P, select):
     (4, 128, 24, 40, 1, "topn", "positions"),
     (4, 128, 24, 40, 1, "cdf", "encoded"),
     (16, 128, 12, 20, 1, "cdf", "encoded"),
+    (8, 256, 16, 24, 1, "cdf", "encoded"),
+    (4, 192, 24, 40, 1, "cdf", "positions"),
 ])
 def test_fp8_variants(N, B, H, W, P, select, din):
     """fp8 path against the oracle's fp8 network (same rounding points: E4M3
