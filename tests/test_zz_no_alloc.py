@@ -24,10 +24,15 @@ def _render(r, fn, poses, H, W, N):
     return rgb.cpu().numpy(), depth.cpu().numpy()
 
 
-@pytest.mark.parametrize("precision,N", [("bf16", 4), ("fp32", 8), ("fp8", 16)])
-def test_static_scratch_matches_render(precision, N):
+@pytest.mark.parametrize("precision,N,B,select", [
+    ("bf16", 4, 128, "topn"), ("fp32", 8, 128, "topn"), ("fp8", 16, 128, "topn"),
+    # the two-sweep inverse-CDF kernel (the depth head streamed twice)
+    ("bf16", 8, 256, "cdf"),
+])
+def test_static_scratch_matches_render(precision, N, B, select):
     prec = {"bf16": b.BF16, "fp32": b.FP32, "fp8": b.FP8}[precision]
-    r = b.Renderer(b.Config(n_bins=128, n_max=N, precision=prec), inputs.make_weights(128, 0))
+    sel = b.SELECT_CDF if select == "cdf" else b.SELECT_TOPN
+    r = b.Renderer(b.Config(n_bins=B, n_max=N, precision=prec, select=sel), inputs.make_weights(B, 0))
     # 2 x 96 x 80 rays: 60 (bf16, fp8) or 120 (fp32) tiles, a partial round
     # split by samples; then 1 x 33 x 29 rays: 4 or 8 tiles, split again
     for poses, H, W in ((inputs.make_poses([0, 3]), 96, 80), (inputs.make_poses([5]), 33, 29)):
