@@ -237,6 +237,31 @@ def test_deterministic_and_plain_render_matches_debug():
     r.close()
 
 
+@pytest.mark.parametrize("precision,select,B,N", [("bf16", "topn", 128, 4), ("fp8", "topn", 256, 8),
+                                                  ("bf16", "cdf", 256, 4)])
+def test_batching_invariance(precision, select, B, N):
+    """A ray's result does not depend on the launch it is in.  Three views of
+    150 x 150 rendered together fill more than one round of 256 tiles and
+    split only the last 8 tiles N ways; each view alone is 88 tiles, all
+    split 2 ways by samples.  Every ray so sits in another tile, another
+    workgroup and mostly another split.  The depth network and the selection
+    (scores, classes, sample depths and widths) are bit-identical; the colour
+    and depth may differ only by the order in which a split ray's parts are
+    composited (a few fp32 ulp)."""
+    sel = b.SELECT_CDF if select == "cdf" else b.SELECT_TOPN
+    r, _ = renderer(precision, n_bins=B, n_max=N, select=sel, seed=2)
+    poses = inputs.make_poses([7, 8, 9])
+    H, W = 150, 150
+    together = gpu_render(r, poses, H, W, N)
+    for i in range(len(poses)):
+        alone = gpu_render(r, poses[i:i + 1], H, W, N)
+        for k in ("scores", "bins", "samples"):
+            assert np.array_equal(alone[k].reshape(-1), together[k][i].reshape(-1)), (i, k)
+        np.testing.assert_allclose(alone["rgb"], together["rgb"][i:i + 1], rtol=0, atol=4e-6)
+        np.testing.assert_allclose(alone["depth"], together["depth"][i:i + 1], rtol=0, atol=2e-5)
+    r.close()
+
+
 def test_render_rejects_bad_sample_count():
     r, _ = renderer("bf16", n_max=4)
     poses = inputs.make_poses([0])
