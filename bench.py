@@ -130,9 +130,11 @@ def cpu_baseline(wl, weights, poses, n_sample):
     return {"value": rate / 1e6, "unit": "Mrays/s", "cores": int(threads), "kind": "oracle",
             "extrapolated": len(sub) < total,
             "s_per_frame": round(wl.H * wl.W / rate, 2),
-            "sample": f"{len(sub)} rays drawn uniformly (seed 1234) from the {wl.n_poses} x {wl.H} x "
-                      f"{wl.W} workload, {wl.precision}-rounding oracle, {dt:.1f} s; the frame time is "
-                      f"extrapolated from it; os.cpu_count()={os.cpu_count()}"}
+            "sample": (f"{len(sub)} rays drawn uniformly (seed 1234) from the {wl.n_poses} x {wl.H} x "
+                       f"{wl.W} workload, {wl.precision}-rounding oracle, {dt:.1f} s; the frame time is "
+                       f"extrapolated from it" if len(sub) < total else
+                       f"all {total} rays of the {wl.n_poses} x {wl.H} x {wl.W} workload, "
+                       f"{wl.precision}-rounding oracle, {dt:.1f} s") + f"; os.cpu_count()={os.cpu_count()}"}
 
 
 def default_cpu_sample(wl):
