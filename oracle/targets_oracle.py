@@ -77,6 +77,8 @@ def neighbourhood_filter(C, K):
             # shifted[y, x] = t[y + i, x + j] where inside the image
             y0, y1 = max(0, -i), min(H, H - i)
             x0, x1 = max(0, -j), min(W, W - j)
+            if y0 >= y1 or x0 >= x1:
+                continue   # the offset leaves the image for every pixel
             out[y0:y1, x0:x1] = np.maximum(out[y0:y1, x0:x1], t[y0 + i:y1 + i, x0 + j:x1 + j])
     return out
 
