@@ -259,9 +259,10 @@ int donerf_debug_mfma_peak(donerf_t* h, int32_t workgroups, int32_t iters, float
  *   Eq. 6  C(z) = 1 for the class z with b_z <= d < b_{z+1} of the pixel's
  *          first-surface depth d (no class where d is outside [d_min, d_max)
  *          or not finite),
- *   Eq. 7  C^(z) = max over the K x K window of C_{x+i,y+j}(z) minus
- *          sqrt(i^2 + j^2) / (sqrt(2) floor(K/2)) (neighbours outside the
- *          image left out; K = 1 keeps C),
+ *   Eq. 7  C^(z) = max over the offsets |i|, |j| <= floor(K/2) of
+ *          C_{x+i,y+j}(z) minus sqrt(i^2 + j^2) / (sqrt(2) floor(K/2))
+ *          (neighbours outside the image left out; K = 1 keeps C; an even
+ *          K spans K + 1 pixels and gives the targets of K + 1),
  *   Eq. 8  C`(z) = min(sum_{|i| <= floor(Z/2)} C^(z + i) (floor(Z/2) + 1 - |i|)
  *          / (floor(Z/2) + 1), 1) (classes outside [0, B) left out).
  *   depth  device, P x H x W fp32: the distance from the camera to the first

@@ -53,9 +53,10 @@ __device__ __forceinline__ int classify(float d, const float* bnd, int B, float 
 
 // CPL: classes per lane (B / 64), lanes own classes CPL lane .. CPL lane +
 // CPL - 1, so each lane writes CPL consecutive targets.  HZ: floor(Z / 2).
-// NM: window entries per lane, ceil(K^2 / 64); fixed at compile time so that
-// a pixel's window reads issue together instead of one guarded read at a
-// time.
+// Eq. 7's offsets run over -floor(K/2) .. floor(K/2), a window of side
+// S = 2 floor(K/2) + 1 (K + 1 for an even K).  NM: window entries per lane,
+// ceil(S^2 / 64); fixed at compile time so that a pixel's window reads issue
+// together instead of one guarded read at a time.
 template <int CPL, int HZ, int NM>
 __global__ void __launch_bounds__(64 * kTgtWaves)
 targets_kernel(const float* __restrict__ depth, int H, int W, const float* __restrict__ bounds, int K,
@@ -93,13 +94,14 @@ targets_kernel(const float* __restrict__ depth, int H, int W, const float* __res
     // Window entries handled by this lane: e = lane + 64 m, offset (i, j).
     // Weights 1 - sqrt(i^2 + j^2) / (sqrt(2) h), in fp64, rounded to fp32
     // (>= 0 inside the window; 1 at the centre, also for K = 1).
-    const int KK = K * K;   // <= 64 NM
+    const int S = 2 * h + 1;
+    const int KK = S * S;   // <= 64 NM
     float wgt[NM];
     int off[NM];
 #pragma unroll
     for (int m = 0; m < NM; ++m) {
         const int e = lane + 64 * m;
-        const int i = e / K - h, j = e % K - h;
+        const int i = e / S - h, j = e % S - h;
         double w = 1.0;
         if (h > 0) w = 1.0 - sqrt((double)(i * i + j * j)) / (sqrt(2.0) * (double)h);
         wgt[m] = fmaxf((float)w, 0.0f);
@@ -202,7 +204,8 @@ namespace {
 template <int CPL, int HZ>
 void launch_cz(dim3 grid, hipStream_t stream, const float* depth, int H, int W, const float* bounds, int K,
                float inv_l2span, float* out) {
-    switch ((K * K + 63) / 64) {   // K <= 15: 1 .. 4
+    const int S = 2 * (K / 2) + 1;   // the window's side, <= 15
+    switch ((S * S + 63) / 64) {     // 1 .. 4
         case 1: hipLaunchKernelGGL((targets_kernel<CPL, HZ, 1>), grid, dim3(64 * kTgtWaves), 0, stream, depth, H, W, bounds, K, inv_l2span, out); break;
         case 2: hipLaunchKernelGGL((targets_kernel<CPL, HZ, 2>), grid, dim3(64 * kTgtWaves), 0, stream, depth, H, W, bounds, K, inv_l2span, out); break;
         case 3: hipLaunchKernelGGL((targets_kernel<CPL, HZ, 3>), grid, dim3(64 * kTgtWaves), 0, stream, depth, H, W, bounds, K, inv_l2span, out); break;

@@ -57,6 +57,16 @@ def test_one_hot_classes_bit_exact(B):
     (128, 11, 1, 1, 13, 29),
     (128, 5, 5, 1, 1, 100),
     (128, 7, 3, 1, 1, 1),
+    # even sizes: the window spans -floor(K/2) .. floor(K/2), K + 1 wide
+    (64, 2, 4, 1, 13, 70),
+    (128, 4, 6, 2, 20, 66),
+    (256, 14, 2, 1, 9, 40),    # side 15: four window entries per lane
+    (192, 8, 12, 1, 17, 33),
+    (128, 10, 5, 1, 1, 90),
+    # windows wider or taller than the image
+    (256, 9, 13, 1, 2, 133),
+    (64, 14, 4, 1, 21, 2),
+    (64, 9, 14, 2, 3, 44),
 ])
 def test_filtered_targets(B, K, Z, P, H, W):
     r = handle(B)
@@ -109,4 +119,17 @@ def test_rejects_bad_windows():
         with pytest.raises(b.DonerfError) as e:
             b.donerf_targets(r.h, d.data_ptr(), P, H, W, 5, 5, out.data_ptr())
         assert e.value.status == b.E_INVALID_ARG, (P, H, W)
+    r.close()
+
+
+@pytest.mark.parametrize("K", [2, 4, 8, 14])
+def test_even_window_equals_next_odd(K):
+    """Eq. 7 depends on K only through floor(K/2): the kernel's targets for
+    an even K are those for K + 1, bit for bit."""
+    r = handle(128)
+    depth = inputs.make_depth_maps(1, 23, 71, seed=K)
+    a = gpu_targets(r, depth, K, 5)
+    c = gpu_targets(r, depth, K + 1, 5)
+    log(f"[targets even K={K}] equal={np.array_equal(a, c)}")
+    assert np.array_equal(a, c)
     r.close()

@@ -63,7 +63,7 @@ def _brute(depth, B, K, Z):
     return out
 
 
-@pytest.mark.parametrize("K,Z", [(1, 1), (3, 3), (5, 5), (5, 1), (1, 5), (9, 3)])
+@pytest.mark.parametrize("K,Z", [(1, 1), (3, 3), (5, 5), (5, 1), (1, 5), (9, 3), (2, 4), (4, 2), (6, 6)])
 def test_brute_force(K, Z):
     rng = np.random.default_rng(K * 10 + Z)
     depth = rng.uniform(0.05, 11.0, size=(6, 7)).astype(F32)   # some below near, some beyond far
@@ -133,3 +133,27 @@ def test_opacity_and_total_loss():
     # mse = 0.01 / 3; mean opacity loss = 0.3125; alpha 1, beta 10 (Sec. 6.1)
     assert abs(T.total_loss(rgb, ref, w) - (0.01 / 3 + 3.125)) < 1e-12
     assert abs(T.total_loss(rgb, ref, w, alpha=2.0, beta=0.0) - 2 * 0.01 / 3) < 1e-12
+
+
+@pytest.mark.parametrize("K", [2, 4, 6, 14])
+def test_even_window_is_the_next_odd_one(K):
+    """Eq. 7 and Eq. 8 see K and Z only through floor(K/2) and floor(Z/2):
+    an even size gives the targets of the odd size above it."""
+    rng = np.random.default_rng(K)
+    depth = rng.uniform(0.05, 11.0, size=(9, 11)).astype(F32)
+    a = T.training_targets(depth, NEAR, FAR, 16, K, K)
+    c = T.training_targets(depth, NEAR, FAR, 16, K + 1, K + 1)
+    assert np.array_equal(a, c)
+    # Eq. 7 alone: the window of K reaches a neighbour that the one of K - 1
+    # (half width one less) does not, so the two differ
+    C = T.one_hot_targets(depth, NEAR, FAR, 16)
+    assert not np.array_equal(T.neighbourhood_filter(C, K), T.neighbourhood_filter(C, K - 1))
+
+
+@pytest.mark.parametrize("H,W,K", [(2, 7, 9), (6, 1, 15), (1, 1, 5), (3, 2, 14)])
+def test_window_larger_than_the_image(H, W, K):
+    """Offsets that leave the image for every pixel contribute nothing."""
+    rng = np.random.default_rng(H * 100 + W * 10 + K)
+    depth = rng.uniform(0.05, 11.0, size=(H, W)).astype(F32)
+    got = T.training_targets(depth, NEAR, FAR, 8, K, 3)
+    np.testing.assert_allclose(got, _brute(depth, 8, K, 3), rtol=0, atol=1e-12)
