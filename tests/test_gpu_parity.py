@@ -37,6 +37,15 @@ PREC = {"fp32": b.FP32, "bf16": b.BF16, "fp8": b.FP8}
 FLIPS = {"fp32": 0.01, "bf16": 0.03, "fp8": 0.05}
 # fp32 scores: a few fp32 roundings of sums of magnitude ~5 (measured 3e-6)
 SCORE_TOL_FP32 = 1e-5
+# depth range and spherical view cell of the default configuration
+GEO = dict(near=0.1, far=10.0, centre=(0.0, 0.0, 0.0), radius=1.5)
+
+
+def geometry(geo):
+    g = dict(GEO)
+    g.update(geo or {})
+    g["centre"] = tuple(float(x) for x in g["centre"])
+    return g
 
 
 def log(*a):
@@ -47,10 +56,13 @@ def log(*a):
 DIN = {"encoded": b.DEPTH_ENCODED, "positions": b.DEPTH_POSITIONS}
 
 
-def renderer(precision, n_bins=128, n_max=4, fov=60.0, select=b.SELECT_TOPN, seed=0, depth_input="encoded"):
+def renderer(precision, n_bins=128, n_max=4, fov=60.0, select=b.SELECT_TOPN, seed=0, depth_input="encoded",
+             geo=None):
     w = inputs.make_weights(n_bins, seed, depth_input)
+    g = geometry(geo)
     cfg = b.Config(n_bins=n_bins, n_max=n_max, precision=PREC[precision], fov_x_deg=fov, select=select,
-                   depth_input=DIN[depth_input])
+                   depth_input=DIN[depth_input], near=g["near"], far=g["far"], centre=g["centre"],
+                   radius=g["radius"])
     return b.Renderer(cfg, w), w
 
 
@@ -60,10 +72,10 @@ def gpu_render(r, poses, H, W, N):
     return {k: v.cpu().numpy() for k, v in out.items()}
 
 
-def _rgbd(rgb, depth):
+def _rgbd(rgb, depth, far=10.0):
     """Per-ray vector of RGB and depth / d_max (depth on the RGB scale)."""
     return np.concatenate([np.asarray(rgb, np.float64).reshape(-1, 3),
-                           np.asarray(depth, np.float64).reshape(-1, 1) / 10.0], axis=1)
+                           np.asarray(depth, np.float64).reshape(-1, 1) / far], axis=1)
 
 
 def check_scores(scores, ora, precision, rerun, label):
@@ -77,22 +89,25 @@ def check_scores(scores, ora, precision, rerun, label):
     log(f"[{label}] scores {st}")
 
 
-def check_colour(rgb, depth, ora, precision, rerun, label):
-    """Teacher-forced RGB and depth of each ray against the oracle."""
+def check_colour(rgb, depth, ora, precision, rerun, label, far=10.0):
+    """Teacher-forced RGB and depth of each ray against the oracle; depth
+    (a weighted sum of sample depths <= d_max) on d_max times the RGB
+    tolerance."""
     err = np.abs(rgb - ora["rgb"]).max()
     derr = np.abs(depth - ora["depth"]).max()
     assert np.all(np.isfinite(rgb)) and np.all((rgb >= 0) & (rgb <= 1))
     if precision in TOL:
         log(f"[{label}] rgb maxabs {err:.3e} depth maxabs {derr:.3e}")
         assert err <= TOL[precision], err
-        assert derr <= 10.0 * TOL[precision], derr
+        assert derr <= far * TOL[precision], derr
     if precision != "fp32":
-        st = validity.check_rays(_rgbd(rgb, depth), _rgbd(ora["rgb"], ora["depth"]), rerun, tol=1e-4, seed=2)
+        st = validity.check_rays(_rgbd(rgb, depth, far), _rgbd(ora["rgb"], ora["depth"], far), rerun, tol=1e-4,
+                                 seed=2)
         log(f"[{label}] rgb+depth {st}")
 
 
 def check_against_oracle(g, w, poses, H, W, N, precision, n_bins=128, fov=60.0, subset=None,
-                         max_flip_frac=0.0, label="", depth_input="encoded", raw_scores=True):
+                         max_flip_frac=0.0, label="", depth_input="encoded", raw_scores=True, geo=None):
     """g: the GPU's per-ray outputs (bins, scores, rgb, depth) of all rays, or
     of ``subset`` (global ray ids) only when they are already that long.
     raw_scores: false when the dumped scores are softmax probabilities."""
@@ -103,13 +118,14 @@ def check_against_oracle(g, w, poses, H, W, N, precision, n_bins=128, fov=60.0, 
     ids = np.arange(len(gb)) if subset is None else np.asarray(subset)
     if len(gb) != len(ids):
         gb, rgb, depth, scores = gb[ids], rgb[ids], depth[ids], scores[ids]
-    kw = dict(n_bins=n_bins, fov_x_deg=fov, precision=precision, depth_input=depth_input)
+    geo = geometry(geo)
+    kw = dict(n_bins=n_bins, fov_x_deg=fov, precision=precision, depth_input=depth_input, **geo)
     ora = O.render(w, poses, H, W, N, forced_bins=gb, ray_subset=ids, **kw)
 
     def rerun(key):
         def f(idx, rng, rho):
             r = O.render(w, poses, H, W, N, forced_bins=gb[idx], ray_subset=ids[idx], jitter=(rng, rho), **kw)
-            return r["logits"] if key == "logits" else _rgbd(r["rgb"], r["depth"])
+            return r["logits"] if key == "logits" else _rgbd(r["rgb"], r["depth"], geo["far"])
         return f
 
     if raw_scores:
@@ -131,7 +147,7 @@ def check_against_oracle(g, w, poses, H, W, N, precision, n_bins=128, fov=60.0, 
             out[gb[r]] = False
             margin = lg[r, gb[r]].min() - lg[r, out].max()
             assert margin >= -2 * SCORE_TOL_FP32, (r, margin)
-    check_colour(rgb, depth, ora, precision, rerun("rgb"), label)
+    check_colour(rgb, depth, ora, precision, rerun("rgb"), label, geo["far"])
     return flips
 
 
@@ -493,7 +509,8 @@ def _log_coord(t, near=0.1, far=10.0):
 CDF_COORD_TOL = 3e-4
 
 
-def check_cdf(g, w, poses, H, W, N, precision, n_bins=128, subset=None, label="", depth_input="encoded"):
+def check_cdf(g, w, poses, H, W, N, precision, n_bins=128, subset=None, label="", depth_input="encoded",
+              fov=60.0, geo=None):
     """Inverse-CDF placement, step by step against the oracle:
     * scores against the oracle's logits, per ray (``check_scores``);
     * the placement on the GPU's own scores (identical inputs) against the
@@ -510,7 +527,9 @@ def check_cdf(g, w, poses, H, W, N, precision, n_bins=128, subset=None, label=""
     ids = np.arange(len(scores)) if subset is None else np.asarray(subset)
     if len(scores) != len(ids):
         scores, samp, cls, rgb, depth = scores[ids], samp[ids], cls[ids], rgb[ids], depth[ids]
-    kw = dict(n_bins=n_bins, precision=precision, select="cdf", depth_input=depth_input)
+    geo = geometry(geo)
+    near, far = geo["near"], geo["far"]
+    kw = dict(n_bins=n_bins, precision=precision, select="cdf", depth_input=depth_input, fov_x_deg=fov, **geo)
     # the depth network and the oracle's own placement
     nat = O.render(w, poses, H, W, N, ray_subset=ids, **kw)
 
@@ -520,18 +539,19 @@ def check_cdf(g, w, poses, H, W, N, precision, n_bins=128, subset=None, label=""
 
     check_scores(scores, nat, precision, rerun_logits, label)
     # the placement on identical scores
-    t_ref, d_ref, c_ref = O.cdf_samples(scores.astype(np.float32), N, 0.1, 10.0)
-    cerr = np.abs(_log_coord(samp[..., 0]) - _log_coord(t_ref)).max()
+    t_ref, d_ref, c_ref = O.cdf_samples(scores.astype(np.float32), N, near, far)
+    cerr = np.abs(_log_coord(samp[..., 0], near, far) - _log_coord(t_ref, near, far)).max()
     werr = np.abs(samp[..., 1] - d_ref).max()
-    wtol = 2 * CDF_COORD_TOL * np.log(10.0 - 0.1 + 1.0) * 10.9
+    # dt/ds of the inverse of Eq. 3 is at most log(D + 1) (D + 1), D = d_max - d_min
+    wtol = 2 * CDF_COORD_TOL * np.log(far - near + 1.0) * (far - near + 1.0)
     log(f"[{label}] placement on the GPU's scores: coord maxabs {cerr:.3e} width maxabs {werr:.3e}")
     assert np.all(np.diff(samp[..., 0], axis=1) >= 0)
-    np.testing.assert_allclose(samp[..., 1].sum(1), float(np.float32(10.0)) - float(np.float32(0.1)), rtol=1e-4)
+    np.testing.assert_allclose(samp[..., 1].sum(1), float(np.float32(far)) - float(np.float32(near)), rtol=1e-4)
     assert cerr <= CDF_COORD_TOL, cerr
     assert werr <= wtol, werr
     if precision == "fp32":
-        s_nat = _log_coord(nat["t"])
-        nerr = np.abs(_log_coord(samp[..., 0]) - s_nat).max()
+        s_nat = _log_coord(nat["t"], near, far)
+        nerr = np.abs(_log_coord(samp[..., 0], near, far) - s_nat).max()
         # classes must agree unless the oracle's sample sits within the
         # coordinate tolerance of a class bound (k / B)
         frac = s_nat * n_bins - np.floor(s_nat * n_bins)
@@ -547,9 +567,9 @@ def check_cdf(g, w, poses, H, W, N, precision, n_bins=128, subset=None, label=""
     def rerun_rgb(idx, rng, rho):
         r = O.render(w, poses, H, W, N, ray_subset=ids[idx], jitter=(rng, rho),
                      forced_samples=(samp[idx, :, 0], samp[idx, :, 1]), **kw)
-        return _rgbd(r["rgb"], r["depth"])
+        return _rgbd(r["rgb"], r["depth"], far)
 
-    check_colour(rgb, depth, ora, precision, rerun_rgb, label)
+    check_colour(rgb, depth, ora, precision, rerun_rgb, label, far)
 
 
 @pytest.mark.parametrize("precision", ["fp32", "bf16"])
