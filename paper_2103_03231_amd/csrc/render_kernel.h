@@ -333,7 +333,11 @@ __device__ __forceinline__ void emit_fp8(const f32x16& a0, const f32x16& a1, u32
         const float v1 = __builtin_amdgcn_fmed3f(v[i + 1], 0.0f, 448.0f);
         const float v2 = __builtin_amdgcn_fmed3f(v[i + 2], 0.0f, 448.0f);
         const float v3 = __builtin_amdgcn_fmed3f(v[i + 3], 0.0f, 448.0f);
-        uint32_t x = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(v0, v1, 0, false);
+        // The convert writes one half of its tied operand and keeps the
+        // other; the second convert overwrites the half this one keeps, so
+        // the operand may be any register: v0's, which dies here, rather
+        // than a zero that costs a move per word.
+        uint32_t x = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(v0, v1, __builtin_bit_cast(int, v0), false);
         x = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(v2, v3, (int)x, true);
         d[w] = x;
     }
