@@ -345,6 +345,39 @@ def test_render_on_a_side_stream():
     r.close()
 
 
+def test_two_handles_on_two_streams():
+    """Each handle owns its weights and split-tail scratch: two handles (bf16
+    B = 128 and fp8 B = 256) rendering at once on two streams, each frame
+    large enough for a split tail, equal their one-at-a-time results bit for
+    bit."""
+    ra, _ = renderer("bf16", n_max=4)
+    rb, _ = renderer("fp8", n_bins=256, n_max=8, seed=3)
+    pa, pb = inputs.make_poses([4, 5, 6]), inputs.make_poses([7, 8])
+    ref_a = ra.render(pa, 150, 170, 4, depth=True)
+    ref_b = rb.render(pb, 160, 150, 8, depth=True)
+    torch.cuda.synchronize()
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    out_a = ra.alloc(3, 150, 170, 4, depth=True)
+    out_b = rb.alloc(2, 160, 150, 8, depth=True)
+    for s, out in ((sa, out_a), (sb, out_b)):
+        with torch.cuda.stream(s):
+            out["rgb"].fill_(-1.0)
+            out["depth"].fill_(-1.0)
+    b.donerf_set_stream(ra.h, sa.cuda_stream)
+    b.donerf_set_stream(rb.h, sb.cuda_stream)
+    for _ in range(3):
+        ra.render_into(pa, 150, 170, 4, out_a)
+        rb.render_into(pb, 160, 150, 8, out_b)
+    sa.synchronize()
+    sb.synchronize()
+    b.donerf_set_stream(ra.h, torch.cuda.current_stream().cuda_stream)
+    b.donerf_set_stream(rb.h, torch.cuda.current_stream().cuda_stream)
+    assert torch.equal(out_a["rgb"], ref_a["rgb"]) and torch.equal(out_a["depth"], ref_a["depth"])
+    assert torch.equal(out_b["rgb"], ref_b["rgb"]) and torch.equal(out_b["depth"], ref_b["depth"])
+    ra.close()
+    rb.close()
+
+
 def test_render_rejects_bad_sizes():
     """Empty frames and frames beyond the stated limits (P H W < 2^31,
     H W <= 2^24) fail before any launch; the Python owner rejects output
