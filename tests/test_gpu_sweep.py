@@ -3,11 +3,15 @@ with the same per-ray rules as the fixed parity tests: precision, placement,
 number of classes, samples per ray, frame shape, poses, weights and depth
 input drawn from a seeded generator, so that combinations the fixed cases do
 not name are covered too.  Frames of up to 2 x 90 x 90 rays span several
-tiles and the split tail; the larger ones are checked on sampled rays."""
+tiles and the split tail; the larger ones are checked on sampled rays.  A
+second set draws the softmax selection and N below n_max too, and checks
+that the plain, debug and allocation-free entry points agree bit for bit."""
 import numpy as np
 import pytest
+import torch
 
 import test_gpu_parity as T
+from oracle import donerf_oracle as O
 from paper_2103_03231_amd import binding as b
 from paper_2103_03231_amd import inputs
 
@@ -47,3 +51,56 @@ def test_random_configuration(i):
         T.check_against_oracle(g, w, poses, H, W, N, c["prec"], n_bins=c["B"], subset=sub, label=label,
                                max_flip_frac=T.FLIPS[c["prec"]] if sub is None or c["prec"] == "fp32" else 0.25,
                                depth_input=c["din"])
+
+
+def _entry_case(i):
+    rng = np.random.default_rng(3000 + i)
+    prec = str(rng.choice(["fp32", "bf16", "fp8"]))
+    select = str(rng.choice(["topn", "softmax", "cdf"]))
+    B = int(rng.choice([64, 128, 192, 256]))
+    din = str(rng.choice(["encoded", "positions"]))
+    n_max = int(rng.integers(1, 17))
+    N = int(rng.integers(1, n_max + 1))
+    P = int(rng.integers(1, 3))
+    H, W = int(rng.integers(1, 61)), int(rng.integers(1, 61))
+    return dict(prec=prec, select=select, B=B, din=din, n_max=n_max, N=N, P=P, H=H, W=W,
+                wseed=int(rng.integers(0, 1000)), pseeds=[int(x) for x in rng.integers(0, 1000, P)])
+
+
+@pytest.mark.parametrize("i", range(12))
+def test_entry_points_agree(i):
+    """The plain, debug and allocation-free renders of one random
+    configuration (softmax selection and N below n_max included, frames down
+    to one pixel) agree bit for bit, and the debug outputs meet the oracle
+    rules; softmax probabilities are checked against a top-N twin handle."""
+    c = _entry_case(i)
+    T.log(f"[entry points {i}] {c}")
+    sel = {"topn": b.SELECT_TOPN, "softmax": b.SELECT_TOPN_SOFTMAX, "cdf": b.SELECT_CDF}[c["select"]]
+    P, H, W, N, B = c["P"], c["H"], c["W"], c["N"], c["B"]
+    poses = inputs.make_poses(c["pseeds"])
+    r, w = T.renderer(c["prec"], n_bins=B, n_max=c["n_max"], select=sel, seed=c["wseed"], depth_input=c["din"])
+    plain = r.render(poses, H, W, N, depth=True)
+    torch.cuda.synchronize()
+    plain = {k: v.cpu().numpy() for k, v in plain.items()}
+    g = T.gpu_render(r, poses, H, W, N)
+    rgb = torch.full((P, H, W, 3), -1.0, dtype=torch.float32, device="cuda")
+    dep = torch.full((P, H, W), -1.0, dtype=torch.float32, device="cuda")
+    b.donerf_render_static_scratch(r.h, poses, P, H, W, N, rgb.data_ptr(), dep.data_ptr())
+    torch.cuda.synchronize()
+    r.close()
+    assert np.array_equal(plain["rgb"], g["rgb"]) and np.array_equal(plain["depth"], g["depth"])
+    assert np.array_equal(plain["rgb"], rgb.cpu().numpy()) and np.array_equal(plain["depth"], dep.cpu().numpy())
+    label = f"entry points {i}"
+    if c["select"] == "cdf":
+        T.check_cdf(g, w, poses, H, W, N, c["prec"], n_bins=B, label=label, depth_input=c["din"])
+        return
+    if c["select"] == "softmax":
+        rt, _ = T.renderer(c["prec"], n_bins=B, n_max=c["n_max"], seed=c["wseed"], depth_input=c["din"])
+        gt = T.gpu_render(rt, poses, H, W, N)
+        rt.close()
+        assert np.array_equal(gt["bins"], g["bins"]) and np.array_equal(gt["rgb"], g["rgb"])
+        np.testing.assert_allclose(g["scores"].reshape(-1, B), O.softmax_fp32(gt["scores"].reshape(-1, B)),
+                                   rtol=1e-5, atol=1e-8)
+        g = gt
+    T.check_against_oracle(g, w, poses, H, W, N, c["prec"], n_bins=B, label=label,
+                           max_flip_frac=T.FLIPS[c["prec"]], depth_input=c["din"])
