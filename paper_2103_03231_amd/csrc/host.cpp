@@ -195,18 +195,23 @@ std::vector<float> fold_positions_layer(const float* W, int B, bool bf16, const 
 }
 
 // Logical input column of the blob for K step ks, lane group g, element e of
-// a layer whose steps have precision p.
-int in_col(int p, int kind, int ks, int g, int e) {
+// a layer whose steps have precision p, in a network of precision net; hidx:
+// the layer's position among its network's hidden layers (-1 for others).
+// In bf16 networks (hid16) the hidden layers take 16x16 steps, and the
+// heads read the 32x32 layout the swap after the last hidden layer restores.
+int in_col(int p, int net, int kind, int hidx, int ks, int g, int e) {
     const int E = elems(p);
     switch (kind) {
         case kDFirst: return d_feature(g, ks * E + e);
         case kDFirstPos: return p_feature(ks, g, e);
         case kSFirst: return s_feature(g, ks * E + e);
         case kHiddenL:
-        case kDHead: return chained_row(p, ks, g, e);
+            if (hid16(net)) return hidx == 0 ? chained16_from32(ks, g, e) : chained16(ks, g, e);
+            return chained_row(p, ks, g, e);
+        case kDHead: return hid16(net) ? chained32_from16(ks, g, e) : chained_row(p, ks, g, e);
         default: {  // kSHead: chained hidden units, then the direction skip
             const int ksh = ksteps(p, kHidden);
-            if (ks < ksh) return chained_row(p, ks, g, e);
+            if (ks < ksh) return hid16(net) ? chained32_from16(ks, g, e) : chained_row(p, ks, g, e);
             const int f = skip_feature(g, (ks - ksh) * E + e);
             return f < 0 ? -1 : kHidden + f;
         }
@@ -216,24 +221,32 @@ int in_col(int p, int kind, int ks, int g, int e) {
 // Append one layer's steps, in the order the kernel consumes them (pass,
 // K step, row block within the pass), padded to whole chunks.  prec: the
 // layer's step precision (layout.h frag_prec); net: the network's (for the
-// chunk count); s: power-of-two scale of fp8 weights (W 2^s is rounded).
-void pack_layer(int prec, int net, int kind, int n_bins, const float* W, int s, std::vector<uint8_t>& dst) {
+// chunk count and the hidden layers' step shape); hidx: the layer's position
+// among the hidden layers (-1 for others); s: power-of-two scale of fp8
+// weights (W 2^s is rounded).  A 16x16 hidden layer (hid16) streams passes
+// of four 16-row tiles, each over its eight K steps of 32: lane l holds row
+// 16 tile + l % 16 and lane group l / 16.
+void pack_layer(int prec, int net, int kind, int hidx, int n_bins, const float* W, int s, std::vector<uint8_t>& dst) {
     const LayerGeom lg = layer_geom(kind, n_bins);
-    const int KS = ksteps(prec, lg.kpad);
+    const bool t16 = kind == kHiddenL && hid16(net);
+    const int rows_per = t16 ? 16 : 32, groups = t16 ? 4 : 2;
+    const int KS = t16 ? lg.kpad / 32 : ksteps(prec, lg.kpad);
+    const int RPP = t16 ? 4 : lg.rbp;               // row blocks or tiles per pass
+    const int NP = lg.rb * 32 / rows_per / RPP;      // passes
     const int E = elems(prec), EB = elem_bytes(prec), U = units(prec);
     const size_t start = dst.size();
     dst.resize(start + (size_t)layer_chunks(net, kind, n_bins) * kChunkBytes, 0);
     uint8_t* out = dst.data() + start;
     size_t f = 0;
-    for (int p = 0; p < lg.rb / lg.rbp; ++p)
+    for (int p = 0; p < NP; ++p)
         for (int ks = 0; ks < KS; ++ks)
-            for (int r = 0; r < lg.rbp; ++r, ++f) {
-                const int rb = p * lg.rbp + r;
+            for (int r = 0; r < RPP; ++r, ++f) {
+                const int rb = p * RPP + r;
                 uint8_t* step = out + f * U * kFragBytes;
                 for (int lane = 0; lane < 64; ++lane) {
-                    const int row = 32 * rb + lane % 32, g = lane / 32;
+                    const int row = rows_per * rb + lane % rows_per, g = lane / (64 / groups);
                     for (int e = 0; e < E; ++e) {
-                        const int colx = in_col(prec, kind, ks, g, e);
+                        const int colx = in_col(prec, net, kind, hidx, ks, g, e);
                         const float v = (row < lg.out_rows && colx >= 0) ? W[(size_t)row * lg.in_cols + colx] : 0.0f;
                         // element e: unit (e * EB) / 16, byte (e * EB) % 16 of the lane's 16
                         uint8_t* dstp = step + ((e * EB) / 16) * kFragBytes + lane * 16 + (e * EB) % 16;
@@ -438,13 +451,13 @@ int donerf_create(const donerf_cfg* cfg, const float* weights, size_t n_weights,
             // network uses them: bf16 in bf16 and fp8 networks
             const std::vector<float> folded =
                 fold_positions_layer(weights + off, B, prec != kF32, centres, cfg->far_dist);
-            pack_layer(fp, prec, kind, B, folded.data(), 0, frags);
+            pack_layer(fp, prec, kind, -1, B, folded.data(), 0, frags);
         } else {
-            pack_layer(fp, prec, kind, B, weights + off, s, frags);
+            pack_layer(fp, prec, kind, kind == kHiddenL ? l % 8 - 1 : -1, B, weights + off, s, frags);
         }
         (l < 8 ? n_d_chunks : n_s_chunks) += layer_chunks(prec, kind, B);
         if (l == 7 && wide_cdf(*cfg)) {
-            pack_layer(fp, prec, kind, B, weights + off, s, frags);
+            pack_layer(fp, prec, kind, -1, B, weights + off, s, frags);
             n_d_chunks += layer_chunks(prec, kind, B);
         }
         off += blob_w_count(l, B, cfg->depth_input);

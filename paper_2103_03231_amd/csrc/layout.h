@@ -73,6 +73,27 @@ DN_HD constexpr int chained_row(int p, int ks, int g, int e) {
                            (((ks % (16 / elems(p))) * elems(p) + e) % 4);
 }
 
+// bf16 networks run their six hidden layers on v_mfma_f32_16x16x32_bf16:
+// 16 rows x 32 K per step, lane l holding row (A) or column (B) l % 16 and
+// K elements 8 (l / 16) + e of lane group G = l / 16; the accumulator holds
+// column l % 16, rows 4 G + i in register i.  A wave's 32 rays are two
+// 16-column tiles, and a pass of four 16-row tiles has eight independent
+// accumulation chains in the registers of two 32x32 blocks.  K step u of
+// tile t is register 2 u + t of the 32x32 B operand array, and one
+// v_permlane16_swap of registers 2 u and 2 u + 1 (lane quadrant 1 with 0,
+// 3 with 2) converts between the two layouts in either direction.
+DN_HD constexpr bool hid16(int net) { return net == kBF16; }
+// Hidden unit that feeds 16x16 K step u, lane group G, element e when the
+// previous 16x16 layer's accumulators are chained: row tiles 2 u and 2 u + 1
+// give elements 0-3 and 4-7.
+DN_HD constexpr int chained16(int u, int G, int e) { return 16 * (2 * u + e / 4) + 4 * G + e % 4; }
+// The first hidden layer's input: the 32x32 chained layout after the swap
+// (group G holds 32x32 K step 2 u + G % 2, lane group G / 2).
+DN_HD constexpr int chained16_from32(int u, int G, int e) { return chained_row(kBF16, 2 * u + G % 2, G / 2, e); }
+// A head after the hidden layers reads 32x32 K step ks, lane group g, after
+// the swap back: 16x16 step ks / 2, group 2 g + ks % 2.
+DN_HD constexpr int chained32_from16(int ks, int g, int e) { return chained16(ks / 2, 2 * g + ks % 2, e); }
+
 // Per-lane feature slots.  Each column's features are split between lane
 // groups g = 0 and 1 (lanes l and l+32 serve the same ray); lane slot s of
 // group g sits at K step s / elems, element s % elems.  The maps give the

@@ -448,6 +448,103 @@ __device__ __forceinline__ void hidden_layer(WS& st, int g, BiasAt bias, GetB&& 
     if constexpr (PADDED && (CH & 1)) st.template next<(CH + PAR0) & 1>();
 }
 
+// ------------------------------------------------------------------ 16x16 hidden layers (bf16)
+
+// One v_mfma_f32_16x16x32_bf16 step (layout.h hid16).
+__device__ __forceinline__ f32x4 mma16(const u32x4& a, const u32x4& b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
+                                                   0, 0, 0);
+}
+
+// Exchanges lane quadrant 1 of x with quadrant 0 of y and quadrant 3 of x
+// with quadrant 2 of y (v_permlane16_swap_b32, per register).
+__device__ __forceinline__ void swap16(u32x4& x, u32x4& y) {
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+        const auto r = __builtin_amdgcn_permlane16_swap(x[w], y[w], false, false);
+        x[w] = r[0];
+        y[w] = r[1];
+    }
+}
+
+// The 16 K steps of a 32x32 B operand of one 32-ray block become the eight
+// 16x16 K steps of its two 16-column tiles (step u, tile t in entry 2 u + t),
+// and back: the swap is its own inverse.
+template <int NK, int CB>
+__device__ __forceinline__ void swap_layouts(u32x4 (&h)[NK][CB]) {
+    static_assert(NK >= 16 && CB == 1, "one 32-ray block of 16 bf16 K steps");
+#pragma unroll
+    for (int u = 0; u < 8; ++u) swap16(h[2 * u][0], h[2 * u + 1][0]);
+}
+
+// ReLU and bf16 rounding of a pair (rounding keeps the sign, so a signed
+// 16-bit max with 0 on the packed pair equals rounding the ReLU).
+__device__ __forceinline__ uint32_t relu_bf16x2(float lo, float hi) {
+    typedef short i16x2 __attribute__((ext_vector_type(2)));
+    const i16x2 v = __builtin_bit_cast(i16x2, pack_bf16x2(lo, hi));
+    return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(v, i16x2{0, 0}));
+}
+
+// A 256 -> 256 bf16 ReLU layer on 16x16x32 steps: four passes of four 16-row
+// tiles (one 32 KiB chunk each), each over eight K steps of 32, for the two
+// 16-column tiles, so a pass runs eight independent accumulation chains.  As
+// in hidden_layer, passes alternate between two accumulator sets and the LDS
+// reads run kFragAhead fragments ahead.  G: the lane group (lane / 16).
+// getB(e, 0) returns entry e (16x16 step e / 2, tile e % 2) of the input;
+// out receives the output in the same form.
+template <int PAR0 = 0, class WS, class GetB, int NOUT, int CB>
+__device__ __forceinline__ void hidden_layer16(WS& st, int G, BiasAt bias, GetB&& getB, u32x4 (&out)[NOUT][CB]) {
+    constexpr int KS = 8;            // K steps of 32
+    constexpr int RT = 4;            // 16-row tiles per pass
+    constexpr int PF = KS * RT;      // fragments per pass
+    constexpr int NF = 4 * PF;       // fragments of the layer
+    constexpr int SPC = kChunkFrags; // fragments per chunk
+    constexpr int D = kFragAhead;
+    static_assert(PF == SPC, "a pass is one chunk");
+    f32x4 acc[2][RT][2];
+    u32x4 a[D + 1];
+    auto load_bias = [&](auto PP) {
+        constexpr int q = CV(PP);
+        sfor<RT>([&](auto R) {
+            const f32x4 b = *reinterpret_cast<const f32x4*>(bias.s + (bias.off + 16 * (RT * q + CV(R)) + 4 * G));
+            acc[q & 1][CV(R)][0] = b;
+            acc[q & 1][CV(R)][1] = b;
+        });
+    };
+    // row tiles 2 j and 2 j + 1 of pass p become K step 2 p + j of the next
+    // layer (layout.h chained16)
+    auto epilogue = [&](auto PP) {
+        constexpr int p = CV(PP);
+        sfor<2>([&](auto J) {
+            sfor<2>([&](auto T) {
+                const f32x4& x = acc[p & 1][2 * CV(J)][CV(T)];
+                const f32x4& y = acc[p & 1][2 * CV(J) + 1][CV(T)];
+                out[2 * (2 * p + CV(J)) + CV(T)][0] =
+                    u32x4{relu_bf16x2(x[0], x[1]), relu_bf16x2(x[2], x[3]), relu_bf16x2(y[0], y[1]),
+                          relu_bf16x2(y[2], y[3])};
+            });
+        });
+    };
+    sfor<NF + D>([&](auto S) {
+        constexpr int s = CV(S);
+        if constexpr (s < NF) {
+            if constexpr (s % SPC == 0) st.template next<(s / SPC + PAR0) & 1>();
+            a[s % (D + 1)] = st.template frag<(s / SPC + PAR0) & 1>(s % SPC);
+        }
+        if constexpr (s >= D) {
+            constexpr int f = s - D;
+            constexpr int p = f / PF, w = f % PF, k = w / RT, r = w % RT;
+            if constexpr (w == 0) load_bias(std::integral_constant<int, p>{});
+            sfor<2>([&](auto T) {
+                const u32x4 bk = getB(std::integral_constant<int, 2 * k + CV(T)>{}, std::integral_constant<int, 0>{});
+                acc[p & 1][r][CV(T)] = mma16(a[f % (D + 1)], bk, acc[p & 1][r][CV(T)]);
+            });
+            if constexpr (w == PF - 1) epilogue(std::integral_constant<int, p>{});
+        }
+        __builtin_amdgcn_sched_barrier(0x6);
+    });
+}
+
 // ------------------------------------------------------------------ selection
 
 // Best-first list of (score, class) under the order: higher score first,
@@ -903,6 +1000,16 @@ render_kernel(const RenderArgs a) {
             }
             hidden_layer<kFP8, CB, KS_HID, kFP8, Q>(st, g, bias_l0 + 256 * 4, g0, h1, ws[4]);
             hidden_layer<FP, CB, KS_HID, kFP8, Q>(st, g, bias_l0 + 256 * 5, g1, h0, ws[5]);
+        } else if constexpr (hid16(PR)) {
+            // 16x16 steps: the first layer's output changes layout on the way
+            // in, the last hidden layer's on the way out to the head
+            const int G = lane >> 4;
+            swap_layouts(h0);
+            for (int l = 0; l < 3; ++l) {
+                hidden_layer16<Q>(st, G, bias_l0 + 256 * (2 * l), g0, h1);
+                hidden_layer16<Q>(st, G, bias_l0 + 256 * (2 * l + 1), g1, h0);
+            }
+            swap_layouts(h0);
         } else {
             for (int l = 0; l < 3; ++l) {
                 hidden_layer<PR, CB, KS_HID, PR, Q>(st, g, bias_l0 + 256 * (2 * l), g0, h1);
