@@ -128,12 +128,13 @@ __device__ __forceinline__ void wave_lds_fence() {
 }
 
 constexpr int kChunkVec = kChunkBytes / 16;  // u32x4 per chunk
-// LDS fragment reads in flight, in MFMA steps: bf16 and fp32 steps read
+// LDS fragment reads in flight, in fragments: bf16 and fp32 fragments are
 // one 1 KiB unit, fp8 steps two.  Measured on 5 x 400 x 400, N = 4: 12 bf16
-// steps ahead run 2 % faster than 3 (14 and more spill); fp8 layers run
-// best with 2 (of 2, 3, 4, 6).
+// fragments ahead ran 2 % faster than 3 with 32x32 hidden layers; with the
+// 16x16 hidden layers 10 runs 0.4 % faster than 12 and 14 0.6 % slower; fp8
+// layers run best with 2 (of 2, 3, 4, 6).
 #ifndef DONERF_FRAG_AHEAD
-#define DONERF_FRAG_AHEAD 12
+#define DONERF_FRAG_AHEAD 10
 #endif
 #ifndef DONERF_FRAG_AHEAD_FP8
 #define DONERF_FRAG_AHEAD_FP8 2
