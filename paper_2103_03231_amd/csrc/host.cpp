@@ -210,8 +210,15 @@ int in_col(int p, int net, int kind, int hidx, int ks, int g, int e) {
             return chained_row(p, ks, g, e);
         case kDHead: return hid16(net) ? chained32_from16(ks, g, e) : chained_row(p, ks, g, e);
         default: {  // kSHead: chained hidden units, then the direction skip
+            if (hid16(net)) {
+                // 16x16 steps of 32: the last hidden layer's 16x16 output,
+                // then the skip, swapped from its two 32x32 steps
+                if (ks < 8) return chained16(ks, g, e);
+                const int f = skip_feature(g / 2, (g % 2) * E + e);
+                return f < 0 ? -1 : kHidden + f;
+            }
             const int ksh = ksteps(p, kHidden);
-            if (ks < ksh) return hid16(net) ? chained32_from16(ks, g, e) : chained_row(p, ks, g, e);
+            if (ks < ksh) return chained_row(p, ks, g, e);
             const int f = skip_feature(g, (ks - ksh) * E + e);
             return f < 0 ? -1 : kHidden + f;
         }
@@ -228,11 +235,12 @@ int in_col(int p, int net, int kind, int hidx, int ks, int g, int e) {
 // 16 tile + l % 16 and lane group l / 16.
 void pack_layer(int prec, int net, int kind, int hidx, int n_bins, const float* W, int s, std::vector<uint8_t>& dst) {
     const LayerGeom lg = layer_geom(kind, n_bins);
-    const bool t16 = kind == kHiddenL && hid16(net);
+    const bool t16 = (kind == kHiddenL || kind == kSHead) && hid16(net);
     const int rows_per = t16 ? 16 : 32, groups = t16 ? 4 : 2;
     const int KS = t16 ? lg.kpad / 32 : ksteps(prec, lg.kpad);
-    const int RPP = t16 ? 4 : lg.rbp;               // row blocks or tiles per pass
-    const int NP = lg.rb * 32 / rows_per / RPP;      // passes
+    // row blocks or tiles per pass, passes (a 16x16 shading head is one tile)
+    const int RPP = t16 ? (kind == kSHead ? 1 : 4) : lg.rbp;
+    const int NP = t16 && kind == kSHead ? 1 : lg.rb * 32 / rows_per / RPP;
     const int E = elems(prec), EB = elem_bytes(prec), U = units(prec);
     const size_t start = dst.size();
     dst.resize(start + (size_t)layer_chunks(net, kind, n_bins) * kChunkBytes, 0);

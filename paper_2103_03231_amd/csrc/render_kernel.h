@@ -546,6 +546,48 @@ __device__ __forceinline__ void hidden_layer16(WS& st, int G, BiasAt bias, GetB&
     });
 }
 
+// The shading head of a 16x16 network: one 16-row tile (rows 0..3 = r, g,
+// b, sigma; the rest zero) over nine K steps of 32, the eight of the last
+// hidden layer's 16x16 output h (entries 2 u + t) and the direction skip sk
+// (entries t, swapped into the 16x16 layout), for the two 16-column tiles.
+// A swap of the two tiles' accumulators then puts rows 0..3 of rays 0..31 in
+// registers 0..3 of lanes 0..31, the lanes and registers the 32x32 head left
+// them in.  BASE: 32 times the slot parity of the head's chunk.
+template <int BASE, class WS, int NK, int NS, int CB, class Epi>
+__device__ __forceinline__ void head16(WS& st, int G, BiasAt bias, u32x4 (&h)[NK][CB], u32x4 (&sk)[NS][CB],
+                                       Epi&& epi) {
+    static_assert(NK >= 16 && NS >= 2 && CB == 1, "one 32-ray block");
+    constexpr int KS = 9;
+    constexpr int D = kFragAhead;
+    const f32x4 b = *reinterpret_cast<const f32x4*>(bias.s + (bias.off + 4 * G));
+    f32x4 acc[2] = {b, b};
+    u32x4 a[KS];
+    sfor<KS + D>([&](auto S) {
+        constexpr int s = CV(S);
+        if constexpr (s < KS) {
+            constexpr int idx = BASE + s;
+            if constexpr (idx % kChunkFrags == 0) st.template next<(idx / kChunkFrags) & 1>();
+            a[s] = st.template frag<(idx / kChunkFrags) & 1>(idx % kChunkFrags);
+        }
+        if constexpr (s >= D && s - D < KS) {
+            constexpr int f = s - D;
+            sfor<2>([&](auto T) {
+                if constexpr (f < 8) acc[CV(T)] = mma16(a[f], h[2 * f + CV(T)][0], acc[CV(T)]);
+                else acc[CV(T)] = mma16(a[f], sk[CV(T)][0], acc[CV(T)]);
+            });
+        }
+        __builtin_amdgcn_sched_barrier(0x6);
+    });
+    f32x4 o;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(acc[0][i]), __float_as_uint(acc[1][i]), false,
+                                                        false);
+        o[i] = __uint_as_float(r[0]);
+    }
+    epi(o);
+}
+
 // ------------------------------------------------------------------ selection
 
 // Best-first list of (score, class) under the order: higher score first,
@@ -980,6 +1022,8 @@ render_kernel(const RenderArgs a) {
 #pragma unroll
         for (int ks = 0; ks < KS_SK; ++ks) skip[ks][cb] = P::pack(fs + E * ks);
     }
+    // a 16x16 shading head reads the skip as one K step of its two tiles
+    if constexpr (hid16(PR)) swap16(skip[0][0], skip[1][0]);
     lds_barrier();  // bias_s and bins_s visible
 
     // ---- depth-oracle network
@@ -992,7 +1036,9 @@ render_kernel(const RenderArgs a) {
     // weight scales start at ws; the last one feeds a head in FP
     // (PAR: slot parity of the first chunk; every hidden layer streams an
     // even number of chunks, so it holds for all six)
-    auto hidden6 = [&](auto PAR, BiasAt bias_l0, const int32_t* ws) {
+    // BACK: whether the output returns to the 32x32 layout (the depth head
+    // needs it; the shading head of a 16x16 network reads the 16x16 one)
+    auto hidden6 = [&](auto PAR, BiasAt bias_l0, const int32_t* ws, auto BACK) {
         constexpr int Q = CV(PAR);
         if constexpr (PR == kFP8) {
             for (int l = 0; l < 2; ++l) {
@@ -1003,14 +1049,14 @@ render_kernel(const RenderArgs a) {
             hidden_layer<FP, CB, KS_HID, kFP8, Q>(st, g, bias_l0 + 256 * 5, g1, h0, ws[5]);
         } else if constexpr (hid16(PR)) {
             // 16x16 steps: the first layer's output changes layout on the way
-            // in, the last hidden layer's on the way out to the head
+            // in, the last hidden layer's on the way out to a 32x32 head
             const int G = lane >> 4;
             swap_layouts(h0);
             for (int l = 0; l < 3; ++l) {
                 hidden_layer16<Q>(st, G, bias_l0 + 256 * (2 * l), g0, h1);
                 hidden_layer16<Q>(st, G, bias_l0 + 256 * (2 * l + 1), g1, h0);
             }
-            swap_layouts(h0);
+            if constexpr (CV(BACK)) swap_layouts(h0);
         } else {
             for (int l = 0; l < 3; ++l) {
                 hidden_layer<PR, CB, KS_HID, PR, Q>(st, g, bias_l0 + 256 * (2 * l), g0, h1);
@@ -1023,7 +1069,7 @@ render_kernel(const RenderArgs a) {
         auto gin = [&](auto K, auto C) { return din[CV(K)][CV(C)]; };
         hidden_layer<PR, CB, KS_D0, DIN == kDinEncoded ? FP : kF32>(st, g, BiasAt{bias_s, 0}, gin, h0);
     }
-    hidden6(std::integral_constant<int, 0>{}, BiasAt{bias_s, 256}, a.wscale + 1);
+    hidden6(std::integral_constant<int, 0>{}, BiasAt{bias_s, 256}, a.wscale + 1, std::true_type{});
     // Head of the depth network: B / 64 passes of 64 classes (32 * kRbPerPass).
     const int npass = a.B / (32 * kRbPerPass);
     constexpr int PASS_FRAGS = KS_H * kRbPerPass;
@@ -1314,28 +1360,40 @@ render_kernel(const RenderArgs a) {
             auto gs = [&](auto K, auto C) { return sin_[CV(K)][CV(C)]; };
             hidden_layer<PR, CB, KS_S0, FP, 0, layer_even_padded(kSFirst)>(st, g, BiasAt{bias_s, s_bias}, gs, h0);
         }
-        hidden6(std::integral_constant<int, S0C & 1>{}, BiasAt{bias_s, s_bias + 256}, a.wscale + 9);
-        auto gh = [&](auto K, auto C) {
-            if constexpr (CV(K) < KS_H) return h0[CV(K)][CV(C)];
-            else return skip[CV(K) - KS_H][CV(C)];
+        hidden6(std::integral_constant<int, S0C & 1>{}, BiasAt{bias_s, s_bias + 256}, a.wscale + 9,
+                std::integral_constant<bool, !hid16(PR)>{});
+        // compositing of one sample from its head outputs (r, g, b, sigma)
+        auto composite = [&](auto C, float hr, float hg, float hb, float hs) {
+            constexpr int cb = CV(C);
+            const float cr = sigmoid<FP == kF32>(hr);
+            const float cg = sigmoid<FP == kF32>(hg);
+            const float cbl = sigmoid<FP == kF32>(hb);
+            const float sigma = fmaxf(hs, 0.0f);
+            const float tau = sigma * dk[cb];
+            const float alpha = one_minus_exp_neg<FP == kF32>(tau);
+            const float wgt = T[cb] * alpha;
+            Cr[cb] += wgt * cr;
+            Cg[cb] += wgt * cg;
+            Cb[cb] += wgt * cbl;
+            Dp[cb] += wgt * tk[cb];
+            T[cb] *= exp_neg<FP == kF32>(tau);
         };
-        run_pass<FP, CB, KS_H + KS_SK, 1, kChunkFrags * ((S0C + HIDC) & 1)>(
-            st, g, BiasAt{bias_s, s_bias + 7 * 256}, gh, [&](auto R, auto C, const f32x16& acc) {
-                constexpr int cb = CV(C);
-                // lanes of group 0 hold rows 0..3 = (r, g, b, sigma) in registers 0..3
-                const float cr = sigmoid<FP == kF32>(acc[0]);
-                const float cg = sigmoid<FP == kF32>(acc[1]);
-                const float cbl = sigmoid<FP == kF32>(acc[2]);
-                const float sigma = fmaxf(acc[3], 0.0f);
-                const float tau = sigma * dk[cb];
-                const float alpha = one_minus_exp_neg<FP == kF32>(tau);
-                const float wgt = T[cb] * alpha;
-                Cr[cb] += wgt * cr;
-                Cg[cb] += wgt * cg;
-                Cb[cb] += wgt * cbl;
-                Dp[cb] += wgt * tk[cb];
-                T[cb] *= exp_neg<FP == kF32>(tau);
-            });
+        if constexpr (hid16(PR)) {
+            head16<kChunkFrags * ((S0C + HIDC) & 1)>(st, lane >> 4, BiasAt{bias_s, s_bias + 7 * 256}, h0, skip,
+                                                     [&](const f32x4& o) {
+                                                         composite(std::integral_constant<int, 0>{}, o[0], o[1], o[2], o[3]);
+                                                     });
+        } else {
+            auto gh = [&](auto K, auto C) {
+                if constexpr (CV(K) < KS_H) return h0[CV(K)][CV(C)];
+                else return skip[CV(K) - KS_H][CV(C)];
+            };
+            run_pass<FP, CB, KS_H + KS_SK, 1, kChunkFrags * ((S0C + HIDC) & 1)>(
+                st, g, BiasAt{bias_s, s_bias + 7 * 256}, gh, [&](auto R, auto C, const f32x16& acc) {
+                    // lanes of group 0 hold rows 0..3 = (r, g, b, sigma) in registers 0..3
+                    composite(C, acc[0], acc[1], acc[2], acc[3]);
+                });
+        }
     }
     st.finish();  // no copy into LDS may outlive the workgroup
 
