@@ -72,7 +72,7 @@ __global__ void __launch_bounds__(256) topn_kernel(const float* scores, int32_t 
         int s[NCAP];
         t.ascending(N, s);
         if (g == 0 && valid)
-            for (int k = 0; k < N; ++k) out[(size_t)r * N + k] = pick(s, k);
+            for (int k = 0; k < N; ++k) out[(size_t)r * N + k] = pick<true>(s, k);
     });
 }
 

@@ -663,11 +663,29 @@ struct TopList {
     }
 };
 
-template <int NCAP>
+// Element k of a per-lane array, as a select chain.  PIN: each element
+// first passes through an empty asm that pins it in a VGPR.  Otherwise the
+// compiler folds the selects of array loads into one load at a computed
+// index, the array becomes a per-thread LDS block, and placing each
+// thread's block makes every wave read the workgroup size from the dispatch
+// packet, a scalar load from host memory: pinning the top-N classes took
+// 8,800 cycles off the 5 x 400 x 400 kernel's step from the depth head to
+// the first sample.  The inverse-CDF arrays (pick_f, and the classes there)
+// are left to the compiler: pinned in registers they spill, and those
+// kernels ran 1 % (N = 4) to 5-10 % (N = 16) slower.
+template <bool PIN, int NCAP>
 __device__ __forceinline__ int pick(const int (&s)[NCAP], int k) {
     int r = s[0];
 #pragma unroll
-    for (int q = 1; q < NCAP; ++q) r = k == q ? s[q] : r;
+    for (int q = 1; q < NCAP; ++q) {
+        if constexpr (PIN) {
+            int v = s[q];
+            asm("" : "+v"(v));
+            r = k == q ? v : r;
+        } else {
+            r = k == q ? s[q] : r;
+        }
+    }
     return r;
 }
 
@@ -1314,7 +1332,7 @@ render_kernel(const RenderArgs a) {
         if constexpr (PLACE == kPlaceTopN) {
             // Always a class index for finite scores; clamped so that no
             // sentinel can address outside the class table.
-            const int bin = min(pick(sel[cb], k), a.B - 1);
+            const int bin = min(pick<true>(sel[cb], k), a.B - 1);
             t = bins_s[bin];
             d = bins_s[a.B + bin];
         } else if constexpr (PLACE == kPlaceCdf) {
@@ -1422,7 +1440,7 @@ render_kernel(const RenderArgs a) {
                         a.out_bins[(size_t)rid[cb] * a.N + k] =
                             __float_as_int(cdf_s[wave * kCdfWaveFloats + col * kCdfRayStride + kCdfClass + k]);
                     else
-                        a.out_bins[(size_t)rid[cb] * a.N + k] = pick(sel[cb], k);
+                        a.out_bins[(size_t)rid[cb] * a.N + k] = pick<PLACE == kPlaceTopN>(sel[cb], k);
                 }
             }
             if (a.out_samples && part == 0) {
