@@ -252,12 +252,19 @@ __device__ __forceinline__ f32x16 bias_frag(BiasAt bias, int g) {
     return b;
 }
 
+struct NoSide {
+    template <class F>
+    __device__ __forceinline__ void operator()(F) const {}
+};
+
 // One accumulator pass: RBP output row blocks x CB column blocks over KS K
 // steps.  BASE is the index of the pass's first fragment within its layer;
 // layers start on chunk boundaries, so chunk changes are known statically.
-// D: LDS reads issued this many fragments ahead.
-template <int PR, int CB, int KS, int RBP, int BASE, int D = kFragAhead, class WS, class GetB, class Epi>
-__device__ __forceinline__ void run_pass(WS& st, int g, BiasAt bias, GetB& getB, Epi&& epi) {
+// D: LDS reads issued this many fragments ahead.  side(f) runs after the
+// MFMAs of fragment f: register work that the matrix pipe can cover.
+template <int PR, int CB, int KS, int RBP, int BASE, int D = kFragAhead, class WS, class GetB, class Epi,
+          class Side = NoSide>
+__device__ __forceinline__ void run_pass(WS& st, int g, BiasAt bias, GetB& getB, Epi&& epi, Side&& side = Side{}) {
     using P = Prec<PR>;
     static_assert(P::U == 1, "heads run single-unit steps");
     constexpr int NF = KS * RBP;   // fragments of the pass, in (K step, row block) order
@@ -285,6 +292,7 @@ __device__ __forceinline__ void run_pass(WS& st, int g, BiasAt bias, GetB& getB,
                 const u32x4 bk = getB(std::integral_constant<int, k>{}, C);
                 acc[r][CV(C)] = P::mma(&a[f], &bk, acc[r][CV(C)], 127);
             });
+            side(std::integral_constant<int, f>{});
         }
         __builtin_amdgcn_sched_barrier(0x6);
     });
@@ -616,11 +624,24 @@ struct TopList {
         const uint32_t lo = (ord << 20) | cidx;
         return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
     }
+    // v_max_f64 / v_min_f64 written out: keys are never NaN, where the
+    // library fmax and fmin would first canonicalise their operands (one
+    // more f64 instruction per operand not known to be canonical).
+    __device__ static __forceinline__ double kmax(double a, double b) {
+        double r;
+        asm("v_max_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+        return r;
+    }
+    __device__ static __forceinline__ double kmin(double a, double b) {
+        double r;
+        asm("v_min_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+        return r;
+    }
     __device__ __forceinline__ void insert(double t) {
 #pragma unroll
         for (int k = 0; k < NCAP; ++k) {
-            const double hi = __builtin_fmax(v[k], t);
-            if (k + 1 < NCAP) t = __builtin_fmin(v[k], t);
+            const double hi = kmax(v[k], t);
+            if (k + 1 < NCAP) t = kmin(v[k], t);
             v[k] = hi;
         }
     }
@@ -1115,7 +1136,31 @@ render_kernel(const RenderArgs a) {
     if constexpr (PLACE == kPlaceTopN) {
         TopList<NCAP> top[CB];
         sfor<CB>([&](auto C) { top[CV(C)].init(); });
+        // Within a group, the scores of pass q wait in registers (the hidden
+        // activations h1 are dead here) and enter the lists one per fragment
+        // during the MFMAs of pass q + 1; the group's last pass inserts its
+        // own after its MFMAs.
+        constexpr int PF = KS_H * kRbPerPass;   // fragments per pass
+        static_assert(PF >= 16 * kRbPerPass, "one insertion per fragment covers a pass's scores");
         for (int p0 = 0; p0 < npass; p0 += GP) {
+            f32x16 held[kRbPerPass][CB];
+            int held_p = 0;
+            auto push_held = [&](auto F) {
+                constexpr int f = CV(F);
+                if constexpr (f < 16 * kRbPerPass) {
+                    constexpr int R = f / 16, i = f % 16;
+                    sfor<CB>([&](auto C) {
+                        // The volatile asms hold the insertion at its step: the
+                        // compiler would otherwise move it out of the MFMA
+                        // stream, up to the chunk barrier or down past the pass.
+                        float x = held[R][CV(C)][i];
+                        asm volatile("" : "+v"(x));
+                        top[CV(C)].push(x, 32 * kRbPerPass * held_p + 32 * R + 8 * (i / 4) + (i % 4));
+#pragma unroll
+                        for (int k = 0; k < NCAP; ++k) asm volatile("" : "+v"(top[CV(C)].v[k]));
+                    });
+                }
+            };
             sfor<GP>([&](auto Q) {
                 constexpr int q = CV(Q);
                 const int p = p0 + q;
@@ -1124,15 +1169,28 @@ render_kernel(const RenderArgs a) {
                     if constexpr (f0 % kChunkFrags == 0) {
                         sfor<CPP>([&](auto J) { st.template next<(f0 / kChunkFrags + CV(J)) & 1>(); });
                     }
+                    if constexpr (q > 0) {
+                        if (p == npass) sfor<16 * kRbPerPass>(push_held);   // the last pass's, held
+                    }
                 } else {
-                    run_pass<FP, CB, KS_H, kRbPerPass, q * PASS_FRAGS>(
-                        st, g, BiasAt{bias_s, kDepthHeadBias + 32 * kRbPerPass * p}, g0,
-                        [&](auto R, auto C, const f32x16& acc) {
+                    auto epi = [&](auto R, auto C, const f32x16& acc) {
+                        if constexpr (q + 1 < GP) {
+                            held[CV(R)][CV(C)] = acc;
+                        } else {
                             const int rowb = 32 * kRbPerPass * p + 32 * CV(R);   // + 4 g: rebase below
 #pragma unroll
                             for (int i = 0; i < 16; ++i) top[CV(C)].push(acc[i], rowb + 8 * (i / 4) + (i % 4));
-                            dump_scores(p, CV(R), CV(C), acc);
-                        });
+                        }
+                        dump_scores(p, CV(R), CV(C), acc);
+                    };
+                    if constexpr (q > 0) {
+                        run_pass<FP, CB, KS_H, kRbPerPass, q * PASS_FRAGS>(
+                            st, g, BiasAt{bias_s, kDepthHeadBias + 32 * kRbPerPass * p}, g0, epi, push_held);
+                    } else {
+                        run_pass<FP, CB, KS_H, kRbPerPass, q * PASS_FRAGS>(
+                            st, g, BiasAt{bias_s, kDepthHeadBias + 32 * kRbPerPass * p}, g0, epi);
+                    }
+                    held_p = p;
                 }
             });
         }
